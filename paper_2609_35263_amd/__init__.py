@@ -1,0 +1,224 @@
+"""Chunked-prefill attention over a paged KV cache on AMD MI355X (gfx950).
+
+Thin Python binding of libwavepp_attn.so (C ABI declared in include/wavepp_attn.h).  Every step of
+the computation runs in the library's HIP kernels; this module only marshals arguments: torch
+tensors are passed as device pointers, the stream is torch's current HIP stream.
+
+Per wave:
+    p = plan(...)                       # host: validate the spans, build the work list
+    ws = new_workspace(p)               # device scratch for metadata and split partials
+    plan_upload(p, ws)                  # enqueue the metadata copy
+    append_kv(p, k_new, v_new, k_pool, v_pool, ws)
+    chunked_prefill(p, q, k_pool, v_pool, out, lse, ws)
+"""
+import ctypes
+import os
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libwavepp_attn.so")
+
+WAVEPP_OK = 0
+STATUS_NAMES = {0: "WAVEPP_OK", -1: "WAVEPP_EINVAL", -2: "WAVEPP_EUNSUPPORTED", -3: "WAVEPP_ERANGE",
+                -4: "WAVEPP_EALIAS", -5: "WAVEPP_EPOSITION", -6: "WAVEPP_ENOSPACE", -7: "WAVEPP_EHIP"}
+
+EXPORTED_SYMBOLS = [
+    "wavepp_attn_plan", "wavepp_plan_workspace_bytes", "wavepp_plan_get_info", "wavepp_plan_get_items",
+    "wavepp_attn_plan_upload", "wavepp_attn_append_kv", "wavepp_attn_chunked_prefill", "wavepp_plan_destroy",
+    "wavepp_status_string", "wavepp_last_error",
+]
+
+
+class WaveppError(RuntimeError):
+    def __init__(self, status, detail):
+        self.status = status
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {detail}")
+
+
+class _Shape(ctypes.Structure):
+    _fields_ = [("num_q_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+                ("head_dim_qk", ctypes.c_int32), ("head_dim_v", ctypes.c_int32),
+                ("page_size", ctypes.c_int32), ("num_pages", ctypes.c_int32),
+                ("kv_shared", ctypes.c_int32), ("softmax_scale", ctypes.c_float)]
+
+
+class _Batch(ctypes.Structure):
+    _fields_ = [("num_requests", ctypes.c_int32), ("prefix_lens", ctypes.POINTER(ctypes.c_int32)),
+                ("chunk_lens", ctypes.POINTER(ctypes.c_int32)), ("block_table", ctypes.POINTER(ctypes.c_int32)),
+                ("bt_stride", ctypes.c_int32)]
+
+
+class _Info(ctypes.Structure):
+    _fields_ = [("total_tokens", ctypes.c_int64), ("num_items", ctypes.c_int32),
+                ("num_real_items", ctypes.c_int32), ("num_merge_items", ctypes.c_int32),
+                ("max_splits", ctypes.c_int32), ("rows_per_item", ctypes.c_int32), ("kv_tile", ctypes.c_int32),
+                ("partial_rows", ctypes.c_int64), ("metadata_bytes", ctypes.c_int64),
+                ("workspace_bytes", ctypes.c_int64)]
+
+
+_lib = None
+
+
+def load_library(path: str = None) -> ctypes.CDLL:
+    """Load the built HIP library; raise if it has not been built (there is no fallback path)."""
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    path = path or LIB_PATH
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it first (python -m paper_2609_35263_amd.build)")
+    lib = ctypes.CDLL(path)
+    vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+    lib.wavepp_attn_plan.argtypes = [ctypes.POINTER(_Shape), ctypes.POINTER(_Batch), i32, ctypes.POINTER(vp)]
+    lib.wavepp_attn_plan.restype = ctypes.c_int
+    lib.wavepp_plan_workspace_bytes.argtypes = [vp]
+    lib.wavepp_plan_workspace_bytes.restype = sz
+    lib.wavepp_plan_get_info.argtypes = [vp, ctypes.POINTER(_Info)]
+    lib.wavepp_plan_get_info.restype = ctypes.c_int
+    lib.wavepp_plan_get_items.argtypes = [vp, ctypes.POINTER(i32), i32]
+    lib.wavepp_plan_get_items.restype = ctypes.c_int
+    lib.wavepp_attn_plan_upload.argtypes = [vp, vp, sz, vp]
+    lib.wavepp_attn_plan_upload.restype = ctypes.c_int
+    lib.wavepp_attn_append_kv.argtypes = [vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.wavepp_attn_append_kv.restype = ctypes.c_int
+    lib.wavepp_attn_chunked_prefill.argtypes = [vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.wavepp_attn_chunked_prefill.restype = ctypes.c_int
+    lib.wavepp_plan_destroy.argtypes = [vp]
+    lib.wavepp_plan_destroy.restype = None
+    lib.wavepp_status_string.argtypes = [ctypes.c_int]
+    lib.wavepp_status_string.restype = ctypes.c_char_p
+    lib.wavepp_last_error.argtypes = []
+    lib.wavepp_last_error.restype = ctypes.c_char_p
+    if path == LIB_PATH:
+        _lib = lib
+    return lib
+
+
+def _check(status):
+    if status != WAVEPP_OK:
+        raise WaveppError(status, load_library().wavepp_last_error().decode())
+
+
+class Plan:
+    """A validated wave and its work list (host object owned by the library)."""
+
+    def __init__(self, handle, shape):
+        self._h = ctypes.c_void_p(handle)
+        self.shape = shape
+
+    @property
+    def handle(self):
+        if not self._h:
+            raise ValueError("plan was destroyed")
+        return self._h
+
+    @property
+    def workspace_bytes(self) -> int:
+        return int(load_library().wavepp_plan_workspace_bytes(self.handle))
+
+    def info(self) -> dict:
+        info = _Info()
+        _check(load_library().wavepp_plan_get_info(self.handle, ctypes.byref(info)))
+        return {name: int(getattr(info, name)) for name, _ in _Info._fields_}
+
+    def items(self) -> np.ndarray:
+        n = self.info()["num_items"]
+        buf = np.zeros((max(n, 1), 8), dtype=np.int32)
+        got = load_library().wavepp_plan_get_items(self.handle, buf.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), n)
+        if got < 0:
+            _check(got)
+        return buf[:got]
+
+    def destroy(self):
+        if self._h:
+            load_library().wavepp_plan_destroy(self._h)
+            self._h = ctypes.c_void_p(None)
+
+    def __del__(self):
+        try:
+            self.destroy()
+        except Exception:
+            pass
+
+
+def plan(*, num_q_heads, num_kv_heads, head_dim_qk, head_dim_v, page_size, num_pages, softmax_scale,
+         prefix_lens, chunk_lens, block_table, kv_shared=False, max_splits=0) -> Plan:
+    lib = load_library()
+    prefix = np.ascontiguousarray(prefix_lens, dtype=np.int32)
+    chunk = np.ascontiguousarray(chunk_lens, dtype=np.int32)
+    bt = np.ascontiguousarray(block_table, dtype=np.int32)
+    if bt.ndim != 2:
+        raise ValueError("block_table must be 2-D [num_requests, bt_stride]")
+    if not (prefix.shape == chunk.shape == (bt.shape[0],)):
+        raise ValueError("prefix_lens, chunk_lens and block_table rows must have the same length")
+    shape = _Shape(num_q_heads, num_kv_heads, head_dim_qk, head_dim_v, page_size, num_pages, int(bool(kv_shared)),
+                   float(softmax_scale))
+    p32 = ctypes.POINTER(ctypes.c_int32)
+    batch = _Batch(int(prefix.shape[0]), prefix.ctypes.data_as(p32), chunk.ctypes.data_as(p32),
+                   bt.ctypes.data_as(p32), int(bt.shape[1]))
+    out = ctypes.c_void_p()
+    _check(lib.wavepp_attn_plan(ctypes.byref(shape), ctypes.byref(batch), int(max_splits), ctypes.byref(out)))
+    return Plan(out.value, dict(num_q_heads=num_q_heads, num_kv_heads=num_kv_heads, head_dim_qk=head_dim_qk,
+                                head_dim_v=head_dim_v, page_size=page_size, num_pages=num_pages,
+                                kv_shared=bool(kv_shared), softmax_scale=float(softmax_scale),
+                                total_tokens=int(chunk.sum())))
+
+
+def plan_for(spec, max_splits=0) -> Plan:
+    """Plan a wave described by a workloads.WaveSpec-like object."""
+    return plan(num_q_heads=spec.num_q_heads, num_kv_heads=spec.num_kv_heads, head_dim_qk=spec.head_dim_qk,
+                head_dim_v=spec.head_dim_v, page_size=spec.page_size, num_pages=spec.num_pages,
+                softmax_scale=spec.softmax_scale, prefix_lens=spec.prefix_lens, chunk_lens=spec.chunk_lens,
+                block_table=spec.block_table, kv_shared=spec.kv_shared, max_splits=max_splits)
+
+
+# ------------------------------------------------------------------------------------------------
+# Device calls (torch tensors for memory and the current stream)
+# ------------------------------------------------------------------------------------------------
+
+def _stream(stream):
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _ptr(t, dtype=None, name=""):
+    if t is None:
+        return ctypes.c_void_p(None)
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def new_workspace(p: Plan, device=None):
+    import torch
+    n = max(p.workspace_bytes, 256)
+    return torch.empty(n, dtype=torch.uint8, device=device or "cuda")
+
+
+def plan_upload(p: Plan, workspace, stream=None):
+    _check(load_library().wavepp_attn_plan_upload(p.handle, _ptr(workspace, name="workspace"),
+                                                  workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def append_kv(p: Plan, k_new, v_new, k_pool, v_pool, workspace, stream=None):
+    import torch
+    bf = torch.bfloat16
+    _check(load_library().wavepp_attn_append_kv(
+        p.handle, _ptr(k_new, bf, "k_new"), _ptr(v_new, bf, "v_new"), _ptr(k_pool, bf, "k_pool"),
+        _ptr(v_pool, bf, "v_pool"), _ptr(workspace, name="workspace"),
+        workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def chunked_prefill(p: Plan, q, k_pool, v_pool, out, lse, workspace, stream=None):
+    import torch
+    bf = torch.bfloat16
+    _check(load_library().wavepp_attn_chunked_prefill(
+        p.handle, _ptr(q, bf, "q"), _ptr(k_pool, bf, "k_pool"), _ptr(v_pool, bf, "v_pool"), _ptr(out, bf, "out"),
+        _ptr(lse, torch.float32, "lse"), _ptr(workspace, name="workspace"),
+        workspace.numel() * workspace.element_size(), _stream(stream)))

@@ -1,0 +1,83 @@
+// Internal layout shared by the host planner (host.cpp) and the gfx950 kernels (kernels.hip).
+// Not part of the public ABI.
+#pragma once
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+namespace wavepp {
+
+constexpr uint32_t kMagic = 0x57415650u;   // "WAVP"
+constexpr int kGqaRowsPerItem = 128;       // 4 waves x 32 query rows
+constexpr int kKvTile = 64;                // keys per inner-loop tile
+constexpr int kNumXcd = 8;                 // L2 domains a launch is spread over, round-robin
+constexpr int kMlaRowsPerItem = 64;        // latent kernel: query rows per work item
+constexpr int kMlaKvTile = 32;
+
+// Header at the start of the uploaded metadata.
+struct alignas(16) MetaHeader {
+  uint32_t magic;
+  uint32_t serial;       // plan identity: kernels compare it with the serial they were launched for
+  int32_t num_requests;
+  int32_t num_items;
+  int32_t num_merge;
+  int32_t bt_stride;
+  int32_t pad[2];
+};
+
+// Per-request span.
+struct alignas(16) ReqMeta {
+  int32_t prefix;   // p_r
+  int32_t chunk;    // c_r
+  int32_t cu;       // first packed token of the chunk
+  int32_t bt_row;   // offset of the request's block-table row (= r * bt_stride)
+};
+
+// One workgroup of the attention kernel.
+struct alignas(16) WorkItem {
+  int32_t req;
+  int32_t kv_head;
+  int32_t row0;      // first packed row (token * G + head_in_group)
+  int32_t rows;      // rows in this item (0 = padding item, does nothing)
+  int32_t kv_begin;  // first key position (multiple of the kernel's key tile)
+  int32_t kv_end;    // one past the last key position
+  int32_t part;      // -1: final output; else first fp32 partial row of this split
+  int32_t split;
+};
+
+// One tile whose key range was split: combine `nsplit` partials into the final output.
+struct alignas(16) MergeItem {
+  int32_t req;
+  int32_t kv_head;
+  int32_t row0;
+  int32_t rows;
+  int32_t nsplit;
+  int32_t part;      // partial rows of split s start at part + s * rows
+  int32_t pad[2];
+};
+
+// Everything a launch needs, resolved to device addresses inside the workspace.
+struct DevPlan {
+  const MetaHeader* hdr;
+  const ReqMeta* reqs;
+  const int32_t* bt;
+  const WorkItem* items;
+  const MergeItem* merges;
+  float* opart;          // [partial_rows][head_dim_v]
+  float* lpart;          // [partial_rows]
+  uint32_t serial;
+  int32_t num_requests;
+  int32_t num_items;
+  int32_t num_merge;
+  int64_t total_tokens;
+  int32_t num_q_heads, num_kv_heads, head_dim_qk, head_dim_v, page_size, kv_shared;
+  float softmax_scale;
+};
+
+hipError_t launch_append(const DevPlan& p, const void* k_new, const void* v_new, void* k_pool, void* v_pool,
+                         hipStream_t stream);
+hipError_t launch_attention(const DevPlan& p, const void* q, const void* k_pool, const void* v_pool, void* out,
+                            float* lse, hipStream_t stream);
+hipError_t launch_merge(const DevPlan& p, void* out, float* lse, hipStream_t stream);
+
+}  // namespace wavepp

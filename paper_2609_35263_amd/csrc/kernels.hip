@@ -1,0 +1,404 @@
+// gfx950 (CDNA4) kernels of libwavepp_attn: K/V append into reserved pages, chunked-prefill
+// attention over paged K/V with bf16 MFMA, and the merge of key-range splits.
+//
+// Attention layout (one workgroup = 4 waves = one work item of up to 128 query rows):
+//   * Rows are (token, head-in-group) pairs of one (request, KV head): row = token * G + h, so the
+//     G query heads that share a KV head share every K/V tile loaded into LDS.
+//   * Each wave owns 32 rows.  Logits are computed transposed, S^T = K Q^T, with
+//     v_mfma_f32_32x32x16_bf16: the K tile (from LDS) is the A operand and the wave's Q rows
+//     (kept in registers for the whole loop) are the B operand.  In the 32x32 accumulator each
+//     lane then holds 16 logits of ONE query row, so the softmax row max / row sum are in-lane
+//     reductions plus a single exchange between the two half-waves.
+//   * The exponentiated probabilities are rounded to bf16 and fed straight back as the B operand
+//     of O^T += V^T P^T: the key order inside that contraction is the order in which the
+//     accumulator holds them, so V^T is read from LDS in the matching order (V is stored
+//     transposed in LDS when it is staged).
+//   * K/V tiles of 64 keys are gathered from the pages named by the block table with 16-byte
+//     loads (one page's head slice is contiguous), double-buffered in LDS: the next tile's global
+//     loads are issued before the current tile's MFMAs and written to the other buffer after.
+//   * Online softmax in fp32 (exp2 with the log2(e) factor folded into the scale); masking is by
+//     selection, and K/V rows past the request's last valid position are never loaded (zeros),
+//     so stale or NaN pool slots cannot leak into the output.
+#include <hip/hip_runtime.h>
+
+#include "internal.h"
+
+namespace wavepp {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+__device__ __forceinline__ bool meta_ok(const DevPlan& p) {
+  return p.hdr->magic == kMagic && p.hdr->serial == p.serial;
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// ---------------------------------------------------------------------------------------------
+// Append: token t of request r -> page bt[r][(p_r + i) / B], slot (p_r + i) % B, all KV heads.
+// One thread moves one 16-byte chunk; the flat index runs over (token, kv head, chunk).
+// ---------------------------------------------------------------------------------------------
+template <int DK, int DV>
+__global__ __launch_bounds__(256) void append_kernel(DevPlan p, const uint4* __restrict__ k_new,
+                                                     const uint4* __restrict__ v_new, uint4* __restrict__ k_pool,
+                                                     uint4* __restrict__ v_pool) {
+  if (!meta_ok(p)) return;
+  constexpr int KC = DK / 8, VC = DV / 8, UC = KC + VC;
+  const int Hkv = p.num_kv_heads;
+  const int64_t units = p.total_tokens * Hkv * UC;
+  const int B = p.page_size;
+  for (int64_t u = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; u < units; u += int64_t(gridDim.x) * blockDim.x) {
+    const int64_t per_tok = int64_t(Hkv) * UC;
+    const int t = int(u / per_tok);
+    const int rem = int(u - int64_t(t) * per_tok);
+    const int h = rem / UC;
+    const int c = rem - h * UC;
+    // request holding token t: the last r with cu_r <= t (idle lanes share cu with the next one)
+    int lo = 0, hi = p.num_requests - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (p.reqs[mid].cu <= t) lo = mid; else hi = mid - 1;
+    }
+    const ReqMeta rm = p.reqs[lo];
+    const int pos = rm.prefix + (t - rm.cu);
+    const int64_t page = p.bt[rm.bt_row + pos / B];
+    const int slot = pos % B;
+    if (c < KC) {
+      k_pool[((page * Hkv + h) * B + slot) * KC + c] = k_new[(int64_t(t) * Hkv + h) * KC + c];
+    } else {
+      const int cv = c - KC;
+      v_pool[((page * Hkv + h) * B + slot) * VC + cv] = v_new[(int64_t(t) * Hkv + h) * VC + cv];
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
+// Grouped-query attention, head dim D (64 or 128), page size PAGE (16 or 64).
+// ---------------------------------------------------------------------------------------------
+template <int D, int PAGE>
+__global__ __launch_bounds__(256, 2) void attn_gqa_kernel(DevPlan p, const __bf16* __restrict__ q,
+                                                          const __bf16* __restrict__ kpool,
+                                                          const __bf16* __restrict__ vpool, __bf16* __restrict__ out,
+                                                          float* __restrict__ lse_out) {
+  constexpr int KT = kKvTile;          // 64 keys per tile
+  constexpr int KSTR = D + 8;          // K tile row stride in LDS (elements); pad keeps rows on distinct banks
+  constexpr int VSTR = KT + 4;         // V^T tile row stride in LDS (elements)
+  constexpr int CH = D / 8;            // 16-byte chunks per key row
+  constexpr int KLOADS = KT * CH / 256;
+  constexpr int KPU = (D == 128) ? 4 : 2;   // keys per thread in the transposing V load
+  static_assert((KT / KPU) * CH == 256, "one V unit per thread");
+  static_assert(KLOADS * 256 == KT * CH, "K tile covered exactly");
+  __shared__ __attribute__((aligned(16))) __bf16 ks[2][KT * KSTR];
+  __shared__ __attribute__((aligned(16))) __bf16 vts[2][D * VSTR];
+
+  if (!meta_ok(p)) return;
+  const WorkItem it = p.items[blockIdx.x];
+  if (it.rows <= 0) return;
+  const ReqMeta rm = p.reqs[it.req];
+  const int Hq = p.num_q_heads, Hkv = p.num_kv_heads;
+  const int G = Hq / Hkv;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, col = lane & 31, hf = lane >> 5;
+  const int n_valid = rm.prefix + rm.chunk;
+  const int32_t* __restrict__ bt = p.bt + rm.bt_row;
+  const int64_t head_off = int64_t(it.kv_head) * PAGE * D;      // offset of this KV head inside a page
+  const int64_t page_stride = int64_t(Hkv) * PAGE * D;
+
+  // ---- this lane's query row -----------------------------------------------------------------
+  const int lrow = wave * 32 + col;
+  const bool row_ok = lrow < it.rows;
+  const int prow = it.row0 + (row_ok ? lrow : 0);
+  const int tok = prow / G;
+  const int head = it.kv_head * G + (prow - tok * G);
+  const int limit = rm.prefix + tok;                             // last key this row may see
+  bf16x8 qf[D / 16];
+  {
+    const __bf16* qrow = q + (int64_t(rm.cu + tok) * Hq + head) * D + 8 * hf;
+#pragma unroll
+    for (int s = 0; s < D / 16; ++s) {
+      if (row_ok) qf[s] = *reinterpret_cast<const bf16x8*>(qrow + 16 * s);
+      else qf[s] = bf16x8{};
+    }
+  }
+  const int wrow0 = wave * 32;
+  const bool wave_active = wrow0 < it.rows;
+  const int wrow_last = min(it.rows, wrow0 + 32) - 1;
+  const int wave_min_lim = rm.prefix + (it.row0 + wrow0) / G;
+  const int wave_max_lim = rm.prefix + (it.row0 + max(wrow_last, wrow0)) / G;
+
+  f32x16 oacc[D / 32];
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db) oacc[db] = f32x16{};
+  float m_run = -INFINITY, l_run = 0.0f;
+  const float sl2 = p.softmax_scale * kLog2e;
+
+  // ---- K/V tile staging -----------------------------------------------------------------------
+  uint4 kreg[KLOADS];
+  uint4 vreg[KPU];
+  const int vkg = tid / CH, vcc = tid % CH;          // V unit: keys [vkg*KPU, +KPU), chunk vcc
+  auto load_tile = [&](int tile) {
+    const int kbase = tile * KT;
+#pragma unroll
+    for (int i = 0; i < KLOADS; ++i) {
+      const int c = tid + 256 * i;
+      const int key = c / CH, cc = c % CH;
+      const int j = kbase + key;
+      if (j < n_valid) {
+        const int64_t page = bt[j / PAGE];
+        kreg[i] = *reinterpret_cast<const uint4*>(kpool + page * page_stride + head_off + (j % PAGE) * D + cc * 8);
+      } else {
+        kreg[i] = uint4{0, 0, 0, 0};
+      }
+    }
+#pragma unroll
+    for (int m = 0; m < KPU; ++m) {
+      const int j = kbase + vkg * KPU + m;
+      if (j < n_valid) {
+        const int64_t page = bt[j / PAGE];
+        vreg[m] = *reinterpret_cast<const uint4*>(vpool + page * page_stride + head_off + (j % PAGE) * D + vcc * 8);
+      } else {
+        vreg[m] = uint4{0, 0, 0, 0};
+      }
+    }
+  };
+  auto store_tile = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < KLOADS; ++i) {
+      const int c = tid + 256 * i;
+      const int key = c / CH, cc = c % CH;
+      *reinterpret_cast<uint4*>(&ks[buf][key * KSTR + cc * 8]) = kreg[i];
+    }
+    // transpose: element e of the 8 d-values of keys [vkg*KPU, +KPU) -> V^T row vcc*8 + e
+    const unsigned short* vv[KPU];
+#pragma unroll
+    for (int m = 0; m < KPU; ++m) vv[m] = reinterpret_cast<const unsigned short*>(&vreg[m]);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      __bf16* dst = &vts[buf][(vcc * 8 + e) * VSTR + vkg * KPU];
+      if constexpr (KPU == 4) {
+        uint2 w;
+        w.x = uint32_t(vv[0][e]) | (uint32_t(vv[1][e]) << 16);
+        w.y = uint32_t(vv[2][e]) | (uint32_t(vv[3][e]) << 16);
+        *reinterpret_cast<uint2*>(dst) = w;
+      } else {
+        *reinterpret_cast<uint32_t*>(dst) = uint32_t(vv[0][e]) | (uint32_t(vv[1][e]) << 16);
+      }
+    }
+  };
+
+  const int t_begin = it.kv_begin / KT;
+  const int t_end = (it.kv_end + KT - 1) / KT;
+  load_tile(t_begin);
+  store_tile(0);
+  __syncthreads();
+
+  for (int tile = t_begin; tile < t_end; ++tile) {
+    const int buf = (tile - t_begin) & 1;
+    const bool has_next = tile + 1 < t_end;
+    if (has_next) load_tile(tile + 1);
+    const int kbase = tile * KT;
+    if (wave_active && kbase <= wave_max_lim) {
+      // S^T[key][row] for the 64 keys of the tile, as two 32-key blocks
+      f32x16 sacc[2];
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        sacc[kb] = f32x16{};
+        const __bf16* krow = &ks[buf][(32 * kb + col) * KSTR + 8 * hf];
+#pragma unroll
+        for (int s = 0; s < D / 16; ++s) {
+          const bf16x8 kf = *reinterpret_cast<const bf16x8*>(krow + 16 * s);
+          sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s], sacc[kb], 0, 0, 0);
+        }
+      }
+      // accumulator element r of block kb holds key 32*kb + 8*(r/4) + 4*hf + (r%4)
+      const bool need_mask = (kbase + KT - 1 > wave_min_lim) || (kbase + KT > it.kv_end);
+      if (need_mask) {
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int key = kbase + 32 * kb + 8 * (r >> 2) + 4 * hf + (r & 3);
+            if (key > limit || key >= it.kv_end) sacc[kb][r] = -INFINITY;
+          }
+      }
+      float mx = -INFINITY;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[kb][r]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float m_new = fmaxf(m_run, mx * sl2);
+      const float m_use = (m_new == -INFINITY) ? 0.0f : m_new;
+      const float alpha = fast_exp2(m_run - m_use);
+      float rs = 0.0f;
+      bf16x8 pb[4];
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float e = fast_exp2(fmaf(sacc[kb][r], sl2, -m_use));
+          rs += e;
+          pb[2 * kb + (r >> 3)][r & 7] = static_cast<__bf16>(e);
+        }
+      rs += __shfl_xor(rs, 32);
+      l_run = l_run * alpha + rs;
+      m_run = m_new;
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
+      // O^T[d][row] += V^T[d][key] P^T[key][row]; step t covers keys 16t + 8*(e/4) + 4*hf + (e%4)
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db) {
+        const __bf16* vrow = &vts[buf][(32 * db + col) * VSTR + 4 * hf];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const bf16x4 lo = *reinterpret_cast<const bf16x4*>(vrow + 16 * t);
+          const bf16x4 hi = *reinterpret_cast<const bf16x4*>(vrow + 16 * t + 8);
+          const bf16x8 a = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+          oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[t], oacc[db], 0, 0, 0);
+        }
+      }
+    }
+    if (has_next) store_tile(buf ^ 1);
+    __syncthreads();
+  }
+
+  // ---- epilogue: O = O^T / l, lse = ln(l) + m ---------------------------------------------------
+  if (!row_ok) return;
+  const float inv_l = l_run > 0.0f ? 1.0f / l_run : 0.0f;
+  const float lse_v = l_run > 0.0f ? (m_run + __log2f(l_run)) * kLn2 : -INFINITY;
+  if (it.part < 0) {
+    __bf16* orow = out + (int64_t(rm.cu + tok) * Hq + head) * D;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        bf16x4 v;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) v[k] = static_cast<__bf16>(oacc[db][4 * u + k] * inv_l);
+        *reinterpret_cast<bf16x4*>(orow + 32 * db + 8 * u + 4 * hf) = v;
+      }
+    if (lse_out && hf == 0) lse_out[int64_t(rm.cu + tok) * Hq + head] = lse_v;
+  } else {
+    float* orow = p.opart + int64_t(it.part + lrow) * D;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        f32x4 v;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) v[k] = oacc[db][4 * u + k] * inv_l;
+        *reinterpret_cast<f32x4*>(orow + 32 * db + 8 * u + 4 * hf) = v;
+      }
+    if (hf == 0) p.lpart[it.part + lrow] = lse_v;
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
+// Merge of key-range splits: o = sum_s w_s o_s / sum_s w_s with w_s = exp(lse_s - max lse),
+// lse = max + ln sum_s w_s.  Splits are combined in index order, so results are deterministic.
+// ---------------------------------------------------------------------------------------------
+template <int DV>
+__global__ __launch_bounds__(256) void merge_kernel(DevPlan p, __bf16* __restrict__ out, float* __restrict__ lse_out) {
+  if (!meta_ok(p)) return;
+  const MergeItem mi = p.merges[blockIdx.x];
+  const ReqMeta rm = p.reqs[mi.req];
+  const int Hq = p.num_q_heads, G = Hq / p.num_kv_heads;
+  constexpr int C4 = DV / 4;
+  for (int idx = threadIdx.x; idx < mi.rows * C4; idx += blockDim.x) {
+    const int lrow = idx / C4, c4 = idx - lrow * C4;
+    float mx = -INFINITY;
+    for (int s = 0; s < mi.nsplit; ++s) mx = fmaxf(mx, p.lpart[mi.part + s * mi.rows + lrow]);
+    f32x4 acc = f32x4{};
+    float wsum = 0.0f;
+    for (int s = 0; s < mi.nsplit; ++s) {
+      const int prow = mi.part + s * mi.rows + lrow;
+      const float l = p.lpart[prow];
+      const float w = (l == -INFINITY) ? 0.0f : fast_exp2((l - mx) * kLog2e);
+      if (w != 0.0f) {
+        const f32x4 v = *reinterpret_cast<const f32x4*>(p.opart + int64_t(prow) * DV + 4 * c4);
+        acc += w * v;
+      }
+      wsum += w;
+    }
+    const float inv = 1.0f / wsum;
+    const int row = mi.row0 + lrow;
+    const int tok = row / G;
+    const int head = mi.kv_head * G + (row - tok * G);
+    bf16x4 o;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) o[k] = static_cast<__bf16>(acc[k] * inv);
+    const int64_t orow = int64_t(rm.cu + tok) * Hq + head;
+    *reinterpret_cast<bf16x4*>(out + orow * DV + 4 * c4) = o;
+    if (lse_out && c4 == 0) lse_out[orow] = mx + __logf(wsum);
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
+// Launchers
+// ---------------------------------------------------------------------------------------------
+hipError_t launch_append(const DevPlan& p, const void* k_new, const void* v_new, void* k_pool, void* v_pool,
+                         hipStream_t stream) {
+  const int dk = p.head_dim_qk, dv = p.kv_shared ? 0 : p.head_dim_v;
+  const int64_t units = p.total_tokens * p.num_kv_heads * ((dk + dv) / 8);
+  if (units == 0) return hipSuccess;
+  const int64_t blocks = std::min<int64_t>((units + 255) / 256, 65536);
+  auto kn = static_cast<const uint4*>(k_new);
+  auto vn = static_cast<const uint4*>(v_new);
+  auto kp = static_cast<uint4*>(k_pool);
+  auto vp = static_cast<uint4*>(v_pool);
+  if (dk == 64 && dv == 64)
+    hipLaunchKernelGGL((append_kernel<64, 64>), dim3(blocks), dim3(256), 0, stream, p, kn, vn, kp, vp);
+  else if (dk == 128 && dv == 128)
+    hipLaunchKernelGGL((append_kernel<128, 128>), dim3(blocks), dim3(256), 0, stream, p, kn, vn, kp, vp);
+  else if (dk == 576 && dv == 0)
+    hipLaunchKernelGGL((append_kernel<576, 0>), dim3(blocks), dim3(256), 0, stream, p, kn, vn, kp, vp);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t launch_attention(const DevPlan& p, const void* q, const void* k_pool, const void* v_pool, void* out,
+                            float* lse, hipStream_t stream) {
+  if (p.num_items == 0) return hipSuccess;
+  auto qq = static_cast<const __bf16*>(q);
+  auto kp = static_cast<const __bf16*>(k_pool);
+  auto vp = static_cast<const __bf16*>(v_pool);
+  auto oo = static_cast<__bf16*>(out);
+  const dim3 grid(p.num_items), block(256);
+  if (p.kv_shared) return hipErrorInvalidValue;
+  if (p.head_dim_qk == 128 && p.page_size == 64)
+    hipLaunchKernelGGL((attn_gqa_kernel<128, 64>), grid, block, 0, stream, p, qq, kp, vp, oo, lse);
+  else if (p.head_dim_qk == 128 && p.page_size == 16)
+    hipLaunchKernelGGL((attn_gqa_kernel<128, 16>), grid, block, 0, stream, p, qq, kp, vp, oo, lse);
+  else if (p.head_dim_qk == 64 && p.page_size == 64)
+    hipLaunchKernelGGL((attn_gqa_kernel<64, 64>), grid, block, 0, stream, p, qq, kp, vp, oo, lse);
+  else if (p.head_dim_qk == 64 && p.page_size == 16)
+    hipLaunchKernelGGL((attn_gqa_kernel<64, 16>), grid, block, 0, stream, p, qq, kp, vp, oo, lse);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t launch_merge(const DevPlan& p, void* out, float* lse, hipStream_t stream) {
+  if (p.num_merge == 0) return hipSuccess;
+  auto oo = static_cast<__bf16*>(out);
+  const dim3 grid(p.num_merge), block(256);
+  if (p.head_dim_v == 128)
+    hipLaunchKernelGGL((merge_kernel<128>), grid, block, 0, stream, p, oo, lse);
+  else if (p.head_dim_v == 64)
+    hipLaunchKernelGGL((merge_kernel<64>), grid, block, 0, stream, p, oo, lse);
+  else if (p.head_dim_v == 512)
+    hipLaunchKernelGGL((merge_kernel<512>), grid, block, 0, stream, p, oo, lse);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+}  // namespace wavepp

@@ -1,0 +1,242 @@
+"""Throughput of one wave of paged chunked-prefill attention on one MI355X.
+
+A step is one pass of the whole hot path over one wave: host plan -> metadata upload -> K/V append ->
+attention (-> split merge), once per layer of the workload.  Inputs are resident in HBM before the
+timed region.  Prints ONE JSON line.
+
+    python bench.py [--steps K] [--warmup W] [--config 2|1|3|4|5|6p|small16...] [--no-cpu-baseline]
+
+Metric: attention TFLOP/s (algorithmic FLOP = 2 * Hq * (d_qk + d_v) * sum_r [c_r p_r + c_r (c_r + 1) / 2]
+per layer, exact causal pairs only), new tokens/s, % of the bf16 dense MFMA peak.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6     # 256 CU x 2.4 GHz x 4096 dense bf16 FLOP/clk/CU
+PEAK_HBM_GBS = 8000.0
+METRIC = "chunked-prefill attention TFLOP/s + new tokens/s on 1 GPU; % of bf16 MFMA peak"
+
+
+def flops_alg(spec) -> float:
+    """Algorithmic FLOP of one layer's attention: exact visible pairs x 2 (QK) + 2 (PV) per dim."""
+    return 2.0 * spec.num_q_heads * (spec.head_dim_qk + spec.head_dim_v) * float(spec.pairs().sum())
+
+
+def bytes_alg(spec) -> float:
+    """Algorithmic HBM bytes of one layer: Q + O + the prefix K/V each request reads + the chunk's K/V
+    read once and written once by the append."""
+    T = spec.total_tokens
+    per_tok = (spec.head_dim_qk * 2 if spec.kv_shared
+               else spec.num_kv_heads * (spec.head_dim_qk + spec.head_dim_v) * 2)
+    q = T * spec.num_q_heads * spec.head_dim_qk * 2
+    o = T * spec.num_q_heads * spec.head_dim_v * 2
+    return float(q + o + float(spec.prefix_lens.sum()) * per_tok + 2.0 * T * per_tok)
+
+
+def append_bytes(spec) -> float:
+    per_tok = (spec.head_dim_qk * 2 if spec.kv_shared
+               else spec.num_kv_heads * (spec.head_dim_qk + spec.head_dim_v) * 2)
+    return 2.0 * spec.total_tokens * per_tok
+
+
+def cpu_baseline(spec, tensors, budget_s=12.0):
+    """Time the fp64 oracle (as it stands) on the host cores on a bounded sample of the same wave.
+
+    Small waves (<= 1 TFLOP) are timed whole; larger ones on random (token, head) rows, each over all
+    of its visible keys, with the sample grown until it takes a few seconds.  The append is done
+    beforehand and is not timed.
+    """
+    import numpy as np
+    import oracle
+    import workloads as wl
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    pools = {k: wl.to_bits(tensors[k]) for k in ("k_pool", "v_pool", "k_new", "v_new")}
+    k1, v1 = oracle.append_kv(pools["k_pool"], pools["v_pool"], pools["k_new"], pools["v_new"], spec.prefix_lens,
+                              spec.chunk_lens, spec.block_table, spec.page_size)
+    del pools
+    kw = dict(page_size=spec.page_size, num_kv_heads=spec.num_kv_heads, softmax_scale=spec.softmax_scale,
+              kv_shared=spec.kv_shared, head_dim_v=spec.head_dim_v)
+    total_flop = flops_alg(spec)
+    if total_flop <= 1e12:
+        q = wl.to_bits(tensors["q"])
+        t0 = time.perf_counter()
+        oracle.chunked_prefill(q, k1, v1, spec.prefix_lens, spec.chunk_lens, spec.block_table, **kw)
+        dt = time.perf_counter() - t0
+        flop, n = total_flop, None
+        sample = f"whole {spec.name} wave (all {spec.total_tokens} tokens x {spec.num_q_heads} heads)"
+    else:
+        rng = np.random.default_rng(0)
+        cu = spec.cu_tokens
+        per_row = 2.0 * (spec.head_dim_qk + spec.head_dim_v)
+        n = 16
+        while True:
+            toks = rng.integers(0, spec.total_tokens, n)
+            heads = rng.integers(0, spec.num_q_heads, n)
+            samples = np.stack([toks, heads], 1)
+            qd = {int(t): wl.to_bits(tensors["q"][int(t)]) for t in set(toks.tolist())}
+            r = np.searchsorted(cu, toks, side="right") - 1
+            flop = float(np.sum(per_row * (spec.prefix_lens[r] + (toks - cu[r]) + 1)))
+            t0 = time.perf_counter()
+            oracle.chunked_prefill_rows(qd, k1, v1, spec.prefix_lens, spec.chunk_lens, spec.block_table,
+                                        samples, **kw)
+            dt = time.perf_counter() - t0
+            if dt >= budget_s / 4 or n >= 1 << 14:
+                break
+            n = int(n * min(16.0, max(2.0, budget_s / 2 / max(dt, 1e-3))))
+        sample = f"{n} random (token, head) rows of the {spec.name} wave, each over all its visible keys"
+    return {"value": round(flop / dt / 1e12, 6), "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+            "sample": sample, "seconds": round(dt, 3)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="2")
+    ap.add_argument("--max-splits", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path (see DESIGN.md, sharding)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import paper_2609_35263_amd as wp
+    import workloads as wl
+
+    wp.load_library()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    spec = wl.config(args.config)
+    layers = spec.layers
+    seed = {"1": 1000, "2": 2000, "3": 3000, "4": 4000, "5": 5000, "6p": 6000}.get(str(args.config), 7000)
+    big = flops_alg(spec) > 1e12
+    # layer tensors, resident in HBM; timing runs use zero-filled (not NaN) unused slots
+    per_layer = [wl.make_tensors(spec, seed=seed, device=dev if big else "cpu", poison=False, layer=l)
+                 for l in range(layers)]
+    cpu_layer0 = per_layer[0] if not big else None
+    dl = [{k: (None if v is None else v.to(dev).contiguous()) for k, v in t.items()} for t in per_layer]
+    T = spec.total_tokens
+    outs = [torch.empty((T, spec.num_q_heads, spec.head_dim_v), dtype=torch.bfloat16, device=dev)
+            for _ in range(layers)]
+    lses = [torch.empty((T, spec.num_q_heads), dtype=torch.float32, device=dev) for _ in range(layers)]
+    p0 = wp.plan_for(spec, max_splits=args.max_splits)
+    ws = wp.new_workspace(p0, dev)
+    info = p0.info()
+    stream = torch.cuda.current_stream()
+
+    attn_events = []
+
+    def step(record=False):
+        p = wp.plan_for(spec, max_splits=args.max_splits)
+        wp.plan_upload(p, ws)
+        for l in range(layers):
+            d = dl[l]
+            wp.append_kv(p, d["k_new"], d["v_new"], d["k_pool"], d["v_pool"], ws)
+            if record:
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                wp.chunked_prefill(p, d["q"], d["k_pool"], d["v_pool"], outs[l], lses[l], ws)
+                e1.record(stream)
+                attn_events.append((e0, e1))
+            else:
+                wp.chunked_prefill(p, d["q"], d["k_pool"], d["v_pool"], outs[l], lses[l], ws)
+        return p
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step(record=True)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms_per_step = elapsed * 1e3 / args.steps
+    attn_ms = float(np.mean([a.elapsed_time(b) for a, b in attn_events]))
+
+    # append alone, for its HBM rate (outside the timed region)
+    wp.plan_upload(p0, ws)
+    torch.cuda.synchronize()
+    a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a0.record(stream)
+    for _ in range(5):
+        wp.append_kv(p0, dl[0]["k_new"], dl[0]["v_new"], dl[0]["k_pool"], dl[0]["v_pool"], ws)
+    a1.record(stream)
+    torch.cuda.synchronize()
+    append_ms = a0.elapsed_time(a1) / 5
+
+    f_layer = flops_alg(spec)
+    f_step = f_layer * layers
+    value = f_step / (ms_per_step * 1e-3) / 1e12
+    achieved = f_layer / (attn_ms * 1e-3) / 1e12
+    traffic = None
+    tfile = os.path.join(ROOT, "profiles", f"traffic_{spec.name}.json")
+    if os.path.exists(tfile):
+        try:
+            tj = json.load(open(tfile))
+            if tj.get("kernel_source_hash") == _kernel_hash():
+                traffic = tj.get("bytes_per_launch")
+        except Exception:
+            traffic = None
+    res = {
+        "metric": METRIC,
+        "value": round(value, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{spec.name}: {spec.num_requests} requests, prefix {int(spec.prefix_lens.min())}-"
+                               f"{int(spec.prefix_lens.max())}, chunks {int(spec.chunk_lens.min())}-"
+                               f"{int(spec.chunk_lens.max())} ({T} new tokens), Hq {spec.num_q_heads}, "
+                               f"Hkv {spec.num_kv_heads}, d {spec.head_dim_qk}/{spec.head_dim_v}, page "
+                               f"{spec.page_size}, layers {layers}",
+                   "global_batch": int(spec.num_requests), "new_tokens": int(T), "layers": int(layers),
+                   "parallelism": "none (1 GPU)"},
+        "new_tokens_per_s": round(T * layers / (ms_per_step * 1e-3) / layers, 1),
+        "pct_peak": round(100.0 * value / PEAK_BF16_TFLOPS, 2),
+        "attn_kernel_ms": round(attn_ms, 4),
+        "append_ms": round(append_ms, 4),
+        "append_GBps": round(append_bytes(spec) / (append_ms * 1e-3) / 1e9, 1),
+        "work_items": info["num_items"],
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic,
+                     "kernel": "attn_gqa_kernel" if not spec.kv_shared else "attn_mla_kernel",
+                     "alg_flop_per_launch": f_layer, "alg_bytes_per_launch": bytes_alg(spec)},
+    }
+    if not args.no_cpu_baseline:
+        # the pools were appended to in place on the device; start from the generator's output again
+        fresh = cpu_layer0 if cpu_layer0 is not None else wl.make_tensors(spec, seed=seed, device=dev, poison=False)
+        res["cpu_baseline"] = cpu_baseline(spec, fresh)
+    print(json.dumps(res), flush=True)
+
+
+def _kernel_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("kernels.hip", "host.cpp", "internal.h"):
+        h.update(open(os.path.join(ROOT, "paper_2609_35263_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+if __name__ == "__main__":
+    main()

@@ -30,6 +30,8 @@ typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
@@ -138,80 +140,104 @@ __global__ __launch_bounds__(256, 2) void attn_gqa_kernel(DevPlan p, const __bf1
   const float sl2 = p.softmax_scale * kLog2e;
 
   // ---- K/V tile staging -----------------------------------------------------------------------
-  uint4 kreg[KLOADS];
-  uint4 vreg[KPU];
+  // Physical pages of a tile are looked up one tile ahead (uniform across the workgroup, so these
+  // are scalar loads), and the K/V loads of tile t+1 are issued before the MFMAs of tile t.  Key
+  // positions past the request's last valid slot are clamped to that slot: those rows are finite
+  // copies that the mask gives zero weight, so stale or NaN pool slots are never read.
+  constexpr int PPT = (PAGE >= KT) ? 1 : KT / PAGE;   // pages touched by one tile
+  const int last_block = (n_valid - 1) / PAGE;
+  const __bf16* __restrict__ kpool_h = kpool + head_off;
+  const __bf16* __restrict__ vpool_h = vpool + head_off;
+  // per-thread constant parts of the tile loads
+  uint32_t koff[KLOADS], kkey[KLOADS];
+#pragma unroll
+  for (int i = 0; i < KLOADS; ++i) {
+    const int c = tid + 256 * i;
+    kkey[i] = uint32_t(c / CH);
+    koff[i] = uint32_t((c % CH) * 8);
+  }
   const int vkg = tid / CH, vcc = tid % CH;          // V unit: keys [vkg*KPU, +KPU), chunk vcc
-  auto load_tile = [&](int tile) {
-    const int kbase = tile * KT;
-#pragma unroll
-    for (int i = 0; i < KLOADS; ++i) {
-      const int c = tid + 256 * i;
-      const int key = c / CH, cc = c % CH;
-      const int j = kbase + key;
-      if (j < n_valid) {
-        const int64_t page = bt[j / PAGE];
-        kreg[i] = *reinterpret_cast<const uint4*>(kpool + page * page_stride + head_off + (j % PAGE) * D + cc * 8);
-      } else {
-        kreg[i] = uint4{0, 0, 0, 0};
-      }
-    }
-#pragma unroll
-    for (int m = 0; m < KPU; ++m) {
-      const int j = kbase + vkg * KPU + m;
-      if (j < n_valid) {
-        const int64_t page = bt[j / PAGE];
-        vreg[m] = *reinterpret_cast<const uint4*>(vpool + page * page_stride + head_off + (j % PAGE) * D + vcc * 8);
-      } else {
-        vreg[m] = uint4{0, 0, 0, 0};
-      }
-    }
-  };
-  auto store_tile = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < KLOADS; ++i) {
-      const int c = tid + 256 * i;
-      const int key = c / CH, cc = c % CH;
-      *reinterpret_cast<uint4*>(&ks[buf][key * KSTR + cc * 8]) = kreg[i];
-    }
-    // transpose: element e of the 8 d-values of keys [vkg*KPU, +KPU) -> V^T row vcc*8 + e
-    const unsigned short* vv[KPU];
-#pragma unroll
-    for (int m = 0; m < KPU; ++m) vv[m] = reinterpret_cast<const unsigned short*>(&vreg[m]);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      __bf16* dst = &vts[buf][(vcc * 8 + e) * VSTR + vkg * KPU];
-      if constexpr (KPU == 4) {
-        uint2 w;
-        w.x = uint32_t(vv[0][e]) | (uint32_t(vv[1][e]) << 16);
-        w.y = uint32_t(vv[2][e]) | (uint32_t(vv[3][e]) << 16);
-        *reinterpret_cast<uint2*>(dst) = w;
-      } else {
-        *reinterpret_cast<uint32_t*>(dst) = uint32_t(vv[0][e]) | (uint32_t(vv[1][e]) << 16);
-      }
-    }
-  };
+  u32x4 kreg[KLOADS];
+  u32x4 vreg[KPU];
+  int pg_nxt[PPT];
+
+#define WAVEPP_TILE_PAGES(tile_, pg_)                                                         \
+  _Pragma("unroll") for (int i_ = 0; i_ < PPT; ++i_) pg_[i_] = bt[min((tile_) * (KT / PAGE) + i_, last_block)];
+
+#define WAVEPP_LOAD_TILE(tile_, pg_)                                                                          \
+  {                                                                                                           \
+    const uint32_t kbase_ = uint32_t(tile_) * KT;                                                             \
+    const uint32_t jmax_ = uint32_t(n_valid - 1);                                                             \
+    _Pragma("unroll") for (int i_ = 0; i_ < KLOADS; ++i_) {                                                   \
+      const uint32_t j_ = min(kbase_ + kkey[i_], jmax_);                                                      \
+      const uint32_t pi_ = (j_ - kbase_) / PAGE;                                                              \
+      int page_ = pg_[0];                                                                                     \
+      _Pragma("unroll") for (int q_ = 1; q_ < PPT; ++q_) page_ = (pi_ == uint32_t(q_)) ? pg_[q_] : page_;     \
+      kreg[i_] = *reinterpret_cast<const u32x4*>(kpool_h + int64_t(page_) * page_stride +                    \
+                                                 ((j_ % PAGE) * D + koff[i_]));                               \
+    }                                                                                                         \
+    _Pragma("unroll") for (int m_ = 0; m_ < KPU; ++m_) {                                                      \
+      const uint32_t j_ = min(kbase_ + uint32_t(vkg * KPU + m_), jmax_);                                      \
+      const uint32_t pi_ = (j_ - kbase_) / PAGE;                                                              \
+      int page_ = pg_[0];                                                                                     \
+      _Pragma("unroll") for (int q_ = 1; q_ < PPT; ++q_) page_ = (pi_ == uint32_t(q_)) ? pg_[q_] : page_;     \
+      vreg[m_] = *reinterpret_cast<const u32x4*>(vpool_h + int64_t(page_) * page_stride +                    \
+                                                 ((j_ % PAGE) * D + uint32_t(vcc * 8)));                      \
+    }                                                                                                         \
+  }
+
+  // V^T row (vcc*8 + e) gets element e of the KPU keys; dword w of a 16-byte chunk holds elements 2w
+  // (low half) and 2w+1 (high half), so v_perm pairs the halves of two keys into one dword.
+#define WAVEPP_STORE_TILE(buf_)                                                                            \
+  {                                                                                                        \
+    _Pragma("unroll") for (int i_ = 0; i_ < KLOADS; ++i_)                                                  \
+        *reinterpret_cast<u32x4*>(&ks[buf_][kkey[i_] * KSTR + koff[i_]]) = kreg[i_];                       \
+    _Pragma("unroll") for (int w_ = 0; w_ < 4; ++w_) {                                                     \
+      __bf16* lo_ = &vts[buf_][(vcc * 8 + 2 * w_) * VSTR + vkg * KPU];                                     \
+      const uint32_t lo01_ = __builtin_amdgcn_perm(vreg[1][w_], vreg[0][w_], 0x05040100u);                 \
+      const uint32_t hi01_ = __builtin_amdgcn_perm(vreg[1][w_], vreg[0][w_], 0x07060302u);                 \
+      if constexpr (KPU == 4) {                                                                            \
+        const uint32_t lo23_ = __builtin_amdgcn_perm(vreg[KPU - 1][w_], vreg[KPU - 2][w_], 0x05040100u);   \
+        const uint32_t hi23_ = __builtin_amdgcn_perm(vreg[KPU - 1][w_], vreg[KPU - 2][w_], 0x07060302u);   \
+        *reinterpret_cast<u32x2*>(lo_) = u32x2{lo01_, lo23_};                                              \
+        *reinterpret_cast<u32x2*>(lo_ + VSTR) = u32x2{hi01_, hi23_};                                       \
+      } else {                                                                                             \
+        *reinterpret_cast<uint32_t*>(lo_) = lo01_;                                                         \
+        *reinterpret_cast<uint32_t*>(lo_ + VSTR) = hi01_;                                                  \
+      }                                                                                                    \
+    }                                                                                                      \
+  }
 
   const int t_begin = it.kv_begin / KT;
   const int t_end = (it.kv_end + KT - 1) / KT;
-  load_tile(t_begin);
-  store_tile(0);
+  {
+    int pg_cur[PPT];
+    WAVEPP_TILE_PAGES(t_begin, pg_cur)
+    WAVEPP_TILE_PAGES(t_begin + 1, pg_nxt)
+    WAVEPP_LOAD_TILE(t_begin, pg_cur)
+    WAVEPP_STORE_TILE(0)
+  }
   __syncthreads();
 
   for (int tile = t_begin; tile < t_end; ++tile) {
     const int buf = (tile - t_begin) & 1;
     const bool has_next = tile + 1 < t_end;
-    if (has_next) load_tile(tile + 1);
+    if (has_next) {
+      WAVEPP_LOAD_TILE(tile + 1, pg_nxt)
+      WAVEPP_TILE_PAGES(tile + 2, pg_nxt)
+    }
     const int kbase = tile * KT;
     if (wave_active && kbase <= wave_max_lim) {
       // S^T[key][row] for the 64 keys of the tile, as two 32-key blocks
       f32x16 sacc[2];
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        sacc[kb] = f32x16{};
-        const __bf16* krow = &ks[buf][(32 * kb + col) * KSTR + 8 * hf];
+      for (int kb = 0; kb < 2; ++kb) sacc[kb] = f32x16{};
+      const __bf16* krow = &ks[buf][col * KSTR + 8 * hf];
 #pragma unroll
-        for (int s = 0; s < D / 16; ++s) {
-          const bf16x8 kf = *reinterpret_cast<const bf16x8*>(krow + 16 * s);
+      for (int s = 0; s < D / 16; ++s) {
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+          const bf16x8 kf = *reinterpret_cast<const bf16x8*>(krow + 32 * kb * KSTR + 16 * s);
           sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s], sacc[kb], 0, 0, 0);
         }
       }
@@ -231,10 +257,14 @@ __global__ __launch_bounds__(256, 2) void attn_gqa_kernel(DevPlan p, const __bf1
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[kb][r]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float m_new = fmaxf(m_run, mx * sl2);
+      mx = fmaxf(mx, __shfl_xor(mx, 32)) * sl2;
+      // The reference max only moves when the tile's max exceeds it by more than 2^8, so most tiles
+      // skip rescaling the accumulators; probabilities stay below 256, which bf16/fp32 hold exactly
+      // as well as values below 1.  The final normalization uses the same reference, so the result
+      // does not depend on when it moved.
+      const bool bump = mx > m_run + 8.0f;
+      const float m_new = bump ? mx : m_run;
       const float m_use = (m_new == -INFINITY) ? 0.0f : m_new;
-      const float alpha = fast_exp2(m_run - m_use);
       float rs = 0.0f;
       bf16x8 pb[4];
 #pragma unroll
@@ -246,12 +276,16 @@ __global__ __launch_bounds__(256, 2) void attn_gqa_kernel(DevPlan p, const __bf1
           pb[2 * kb + (r >> 3)][r & 7] = static_cast<__bf16>(e);
         }
       rs += __shfl_xor(rs, 32);
-      l_run = l_run * alpha + rs;
+      if (__any(bump)) {
+        const float alpha = fast_exp2(m_run - m_use);
+        l_run *= alpha;
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
+      }
+      l_run += rs;
       m_run = m_new;
-#pragma unroll
-      for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
       // O^T[d][row] += V^T[d][key] P^T[key][row]; step t covers keys 16t + 8*(e/4) + 4*hf + (e%4)
 #pragma unroll
       for (int db = 0; db < D / 32; ++db) {
@@ -260,14 +294,17 @@ __global__ __launch_bounds__(256, 2) void attn_gqa_kernel(DevPlan p, const __bf1
         for (int t = 0; t < 4; ++t) {
           const bf16x4 lo = *reinterpret_cast<const bf16x4*>(vrow + 16 * t);
           const bf16x4 hi = *reinterpret_cast<const bf16x4*>(vrow + 16 * t + 8);
-          const bf16x8 a = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+          const bf16x8 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
           oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[t], oacc[db], 0, 0, 0);
         }
       }
     }
-    if (has_next) store_tile(buf ^ 1);
+    if (has_next) WAVEPP_STORE_TILE(buf ^ 1)
     __syncthreads();
   }
+#undef WAVEPP_TILE_PAGES
+#undef WAVEPP_LOAD_TILE
+#undef WAVEPP_STORE_TILE
 
   // ---- epilogue: O = O^T / l, lse = ln(l) + m ---------------------------------------------------
   if (!row_ok) return;

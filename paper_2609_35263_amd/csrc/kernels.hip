@@ -11,14 +11,15 @@
 //     reductions plus a single exchange between the two half-waves.
 //   * The exponentiated probabilities are rounded to bf16 and fed straight back as the B operand
 //     of O^T += V^T P^T: the key order inside that contraction is the order in which the
-//     accumulator holds them, so V^T is read from LDS in the matching order (V is stored
-//     transposed in LDS when it is staged).
+//     accumulator holds them.  V is staged in LDS row-major like K and read with gfx950's
+//     transposing LDS load (ds_read_b64_tr_b16) in that matching order.
 //   * K/V tiles of 64 keys are gathered from the pages named by the block table with 16-byte
 //     loads (one page's head slice is contiguous), double-buffered in LDS: the next tile's global
 //     loads are issued before the current tile's MFMAs and written to the other buffer after.
 //   * Online softmax in fp32 (exp2 with the log2(e) factor folded into the scale); masking is by
-//     selection, and K/V rows past the request's last valid position are never loaded (zeros),
-//     so stale or NaN pool slots cannot leak into the output.
+//     selection, and K/V rows past the request's last valid position are never loaded (their
+//     addresses are clamped to the last valid row), so stale or NaN pool slots cannot leak into
+//     the output.
 #include <hip/hip_runtime.h>
 
 #include "internal.h"
@@ -83,21 +84,41 @@ __global__ __launch_bounds__(256) void append_kernel(DevPlan p, const uint4* __r
 // ---------------------------------------------------------------------------------------------
 // Grouped-query attention, head dim D (64 or 128), page size PAGE (16 or 64).
 // ---------------------------------------------------------------------------------------------
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+
+// Both halves of the wave receive max / sum of their value and the other half's value for the
+// same query row (lanes l and l ^ 32).
+__device__ __forceinline__ float halves_max(float x) {
+  const auto s = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(s[0]), __uint_as_float(s[1]));
+}
+__device__ __forceinline__ float halves_sum(float x) {
+  const auto s = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(s[0]) + __uint_as_float(s[1]);
+}
+
+// Transposing LDS read: within each group of 16 lanes, lane i receives element i%4 of the 8 bytes
+// addressed by lanes 4m + i/4, m = 0..3.
+__device__ __forceinline__ bf16x4 lds_read_tr(const __bf16* p) {
+  const i16x4 r = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p));
+  return __builtin_bit_cast(bf16x4, r);
+}
+
 template <int D, int PAGE>
 __global__ __launch_bounds__(256, 2) void attn_gqa_kernel(DevPlan p, const __bf16* __restrict__ q,
                                                           const __bf16* __restrict__ kpool,
                                                           const __bf16* __restrict__ vpool, __bf16* __restrict__ out,
                                                           float* __restrict__ lse_out) {
   constexpr int KT = kKvTile;          // 64 keys per tile
-  constexpr int KSTR = D + 8;          // K tile row stride in LDS (elements); pad keeps rows on distinct banks
-  constexpr int VSTR = KT + 4;         // V^T tile row stride in LDS (elements)
+  constexpr int KSTR = D + 8;          // K rows in LDS: 16-byte reads of 8 rows land on distinct banks
+  constexpr int VSTR = D + 16;         // V rows in LDS: transposed reads of 4 rows x 32 bytes on distinct banks
   constexpr int CH = D / 8;            // 16-byte chunks per key row
-  constexpr int KLOADS = KT * CH / 256;
-  constexpr int KPU = (D == 128) ? 4 : 2;   // keys per thread in the transposing V load
-  static_assert((KT / KPU) * CH == 256, "one V unit per thread");
-  static_assert(KLOADS * 256 == KT * CH, "K tile covered exactly");
+  constexpr int LOADS = KT * CH / 256; // chunks per thread per tile, for K and for V alike
+  constexpr int PPT = (PAGE >= KT) ? 1 : KT / PAGE;   // pages touched by one tile
+  static_assert(LOADS * 256 == KT * CH, "tile covered exactly");
   __shared__ __attribute__((aligned(16))) __bf16 ks[2][KT * KSTR];
-  __shared__ __attribute__((aligned(16))) __bf16 vts[2][D * VSTR];
+  __shared__ __attribute__((aligned(16))) __bf16 vs[2][KT * VSTR];
 
   if (!meta_ok(p)) return;
   const WorkItem it = p.items[blockIdx.x];
@@ -108,8 +129,9 @@ __global__ __launch_bounds__(256, 2) void attn_gqa_kernel(DevPlan p, const __bf1
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, col = lane & 31, hf = lane >> 5;
   const int n_valid = rm.prefix + rm.chunk;
   const int32_t* __restrict__ bt = p.bt + rm.bt_row;
-  const int64_t head_off = int64_t(it.kv_head) * PAGE * D;      // offset of this KV head inside a page
   const int64_t page_stride = int64_t(Hkv) * PAGE * D;
+  const __bf16* __restrict__ kpool_h = kpool + int64_t(it.kv_head) * PAGE * D;
+  const __bf16* __restrict__ vpool_h = vpool + int64_t(it.kv_head) * PAGE * D;
 
   // ---- this lane's query row -----------------------------------------------------------------
   const int lrow = wave * 32 + col;
@@ -122,10 +144,7 @@ __global__ __launch_bounds__(256, 2) void attn_gqa_kernel(DevPlan p, const __bf1
   {
     const __bf16* qrow = q + (int64_t(rm.cu + tok) * Hq + head) * D + 8 * hf;
 #pragma unroll
-    for (int s = 0; s < D / 16; ++s) {
-      if (row_ok) qf[s] = *reinterpret_cast<const bf16x8*>(qrow + 16 * s);
-      else qf[s] = bf16x8{};
-    }
+    for (int s = 0; s < D / 16; ++s) qf[s] = row_ok ? *reinterpret_cast<const bf16x8*>(qrow + 16 * s) : bf16x8{};
   }
   const int wrow0 = wave * 32;
   const bool wave_active = wrow0 < it.rows;
@@ -140,73 +159,53 @@ __global__ __launch_bounds__(256, 2) void attn_gqa_kernel(DevPlan p, const __bf1
   const float sl2 = p.softmax_scale * kLog2e;
 
   // ---- K/V tile staging -----------------------------------------------------------------------
-  // Physical pages of a tile are looked up one tile ahead (uniform across the workgroup, so these
-  // are scalar loads), and the K/V loads of tile t+1 are issued before the MFMAs of tile t.  Key
-  // positions past the request's last valid slot are clamped to that slot: those rows are finite
-  // copies that the mask gives zero weight, so stale or NaN pool slots are never read.
-  constexpr int PPT = (PAGE >= KT) ? 1 : KT / PAGE;   // pages touched by one tile
+  // Thread tid moves 16-byte chunks c = tid + 256 i of both the K and the V tile: key c / CH, chunk
+  // c % CH; consecutive threads read consecutive 16 bytes of a page's contiguous head slice.  The
+  // physical pages of a tile are looked up one tile ahead (uniform across the workgroup, hence
+  // scalar loads) and the loads of tile t+1 are issued before the MFMAs of tile t.  In the last
+  // tile of a request, key positions past its last valid slot are clamped to that slot: those rows
+  // are finite copies that the mask gives zero weight, so stale or NaN pool slots are never read.
   const int last_block = (n_valid - 1) / PAGE;
-  const __bf16* __restrict__ kpool_h = kpool + head_off;
-  const __bf16* __restrict__ vpool_h = vpool + head_off;
-  // per-thread constant parts of the tile loads
-  uint32_t koff[KLOADS], kkey[KLOADS];
+  int ckey[LOADS];
+  uint32_t coff[LOADS];
 #pragma unroll
-  for (int i = 0; i < KLOADS; ++i) {
+  for (int i = 0; i < LOADS; ++i) {
     const int c = tid + 256 * i;
-    kkey[i] = uint32_t(c / CH);
-    koff[i] = uint32_t((c % CH) * 8);
+    ckey[i] = c / CH;
+    coff[i] = uint32_t((c % CH) * 8);
   }
-  const int vkg = tid / CH, vcc = tid % CH;          // V unit: keys [vkg*KPU, +KPU), chunk vcc
-  u32x4 kreg[KLOADS];
-  u32x4 vreg[KPU];
+  u32x4 kreg[LOADS], vreg[LOADS];
   int pg_nxt[PPT];
 
-#define WAVEPP_TILE_PAGES(tile_, pg_)                                                         \
+#define WAVEPP_TILE_PAGES(tile_, pg_)                                                                     \
   _Pragma("unroll") for (int i_ = 0; i_ < PPT; ++i_) pg_[i_] = bt[min((tile_) * (KT / PAGE) + i_, last_block)];
 
-#define WAVEPP_LOAD_TILE(tile_, pg_)                                                                          \
-  {                                                                                                           \
-    const uint32_t kbase_ = uint32_t(tile_) * KT;                                                             \
-    const uint32_t jmax_ = uint32_t(n_valid - 1);                                                             \
-    _Pragma("unroll") for (int i_ = 0; i_ < KLOADS; ++i_) {                                                   \
-      const uint32_t j_ = min(kbase_ + kkey[i_], jmax_);                                                      \
-      const uint32_t pi_ = (j_ - kbase_) / PAGE;                                                              \
-      int page_ = pg_[0];                                                                                     \
-      _Pragma("unroll") for (int q_ = 1; q_ < PPT; ++q_) page_ = (pi_ == uint32_t(q_)) ? pg_[q_] : page_;     \
-      kreg[i_] = *reinterpret_cast<const u32x4*>(kpool_h + int64_t(page_) * page_stride +                    \
-                                                 ((j_ % PAGE) * D + koff[i_]));                               \
-    }                                                                                                         \
-    _Pragma("unroll") for (int m_ = 0; m_ < KPU; ++m_) {                                                      \
-      const uint32_t j_ = min(kbase_ + uint32_t(vkg * KPU + m_), jmax_);                                      \
-      const uint32_t pi_ = (j_ - kbase_) / PAGE;                                                              \
-      int page_ = pg_[0];                                                                                     \
-      _Pragma("unroll") for (int q_ = 1; q_ < PPT; ++q_) page_ = (pi_ == uint32_t(q_)) ? pg_[q_] : page_;     \
-      vreg[m_] = *reinterpret_cast<const u32x4*>(vpool_h + int64_t(page_) * page_stride +                    \
-                                                 ((j_ % PAGE) * D + uint32_t(vcc * 8)));                      \
-    }                                                                                                         \
+#define WAVEPP_LOAD_TILE(tile_, pg_)                                                                      \
+  {                                                                                                       \
+    const int kbase_ = (tile_) * KT;                                                                      \
+    const bool full_ = kbase_ + KT <= n_valid;                                                            \
+    _Pragma("unroll") for (int i_ = 0; i_ < LOADS; ++i_) {                                                \
+      const int j_ = full_ ? kbase_ + ckey[i_] : min(kbase_ + ckey[i_], n_valid - 1);                     \
+      const int sub_ = (j_ - kbase_) / PAGE;                                                              \
+      int page_ = pg_[0];                                                                                 \
+      _Pragma("unroll") for (int q_ = 1; q_ < PPT; ++q_) page_ = (sub_ == q_) ? pg_[q_] : page_;          \
+      const uint32_t off_ = uint32_t(j_ % PAGE) * D + coff[i_];                                           \
+      kreg[i_] = *reinterpret_cast<const u32x4*>(kpool_h + int64_t(page_) * page_stride + off_);         \
+      vreg[i_] = *reinterpret_cast<const u32x4*>(vpool_h + int64_t(page_) * page_stride + off_);         \
+    }                                                                                                     \
   }
 
-  // V^T row (vcc*8 + e) gets element e of the KPU keys; dword w of a 16-byte chunk holds elements 2w
-  // (low half) and 2w+1 (high half), so v_perm pairs the halves of two keys into one dword.
-#define WAVEPP_STORE_TILE(buf_)                                                                            \
-  {                                                                                                        \
-    _Pragma("unroll") for (int i_ = 0; i_ < KLOADS; ++i_)                                                  \
-        *reinterpret_cast<u32x4*>(&ks[buf_][kkey[i_] * KSTR + koff[i_]]) = kreg[i_];                       \
-    _Pragma("unroll") for (int w_ = 0; w_ < 4; ++w_) {                                                     \
-      __bf16* lo_ = &vts[buf_][(vcc * 8 + 2 * w_) * VSTR + vkg * KPU];                                     \
-      const uint32_t lo01_ = __builtin_amdgcn_perm(vreg[1][w_], vreg[0][w_], 0x05040100u);                 \
-      const uint32_t hi01_ = __builtin_amdgcn_perm(vreg[1][w_], vreg[0][w_], 0x07060302u);                 \
-      if constexpr (KPU == 4) {                                                                            \
-        const uint32_t lo23_ = __builtin_amdgcn_perm(vreg[KPU - 1][w_], vreg[KPU - 2][w_], 0x05040100u);   \
-        const uint32_t hi23_ = __builtin_amdgcn_perm(vreg[KPU - 1][w_], vreg[KPU - 2][w_], 0x07060302u);   \
-        *reinterpret_cast<u32x2*>(lo_) = u32x2{lo01_, lo23_};                                              \
-        *reinterpret_cast<u32x2*>(lo_ + VSTR) = u32x2{hi01_, hi23_};                                       \
-      } else {                                                                                             \
-        *reinterpret_cast<uint32_t*>(lo_) = lo01_;                                                         \
-        *reinterpret_cast<uint32_t*>(lo_ + VSTR) = hi01_;                                                  \
-      }                                                                                                    \
-    }                                                                                                      \
+#define WAVEPP_STORE_TILE(buf_)                                                                           \
+  _Pragma("unroll") for (int i_ = 0; i_ < LOADS; ++i_) {                                                  \
+    *reinterpret_cast<u32x4*>(&ks[buf_][ckey[i_] * KSTR + coff[i_]]) = kreg[i_];                          \
+    *reinterpret_cast<u32x4*>(&vs[buf_][ckey[i_] * VSTR + coff[i_]]) = vreg[i_];                          \
   }
+
+  // per-lane LDS read bases.  K (A operand of S^T = K Q^T): row col, elements 8*hf.. of each
+  // 16-wide step.  V (A operand of O^T = V^T P^T, read transposed): within its 16-lane group, lane
+  // j = lane % 16 addresses key 4*hf + j/4 and d = 16*((lane/16) % 2) + 4*(j%4) of a 16-key step.
+  const int k_lane = col * KSTR + 8 * hf;
+  const int v_lane = (4 * hf + (lane & 15) / 4) * VSTR + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
 
   const int t_begin = it.kv_begin / KT;
   const int t_end = (it.kv_end + KT - 1) / KT;
@@ -229,18 +228,15 @@ __global__ __launch_bounds__(256, 2) void attn_gqa_kernel(DevPlan p, const __bf1
     const int kbase = tile * KT;
     if (wave_active && kbase <= wave_max_lim) {
       // S^T[key][row] for the 64 keys of the tile, as two 32-key blocks
-      f32x16 sacc[2];
+      f32x16 sacc[2] = {f32x16{}, f32x16{}};
+      const __bf16* kl = &ks[buf][k_lane];
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) sacc[kb] = f32x16{};
-      const __bf16* krow = &ks[buf][col * KSTR + 8 * hf];
-#pragma unroll
-      for (int s = 0; s < D / 16; ++s) {
+      for (int s = 0; s < D / 16; ++s)
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb) {
-          const bf16x8 kf = *reinterpret_cast<const bf16x8*>(krow + 32 * kb * KSTR + 16 * s);
+          const bf16x8 kf = *reinterpret_cast<const bf16x8*>(kl + 32 * kb * KSTR + 16 * s);
           sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s], sacc[kb], 0, 0, 0);
         }
-      }
       // accumulator element r of block kb holds key 32*kb + 8*(r/4) + 4*hf + (r%4)
       const bool need_mask = (kbase + KT - 1 > wave_min_lim) || (kbase + KT > it.kv_end);
       if (need_mask) {
@@ -257,11 +253,10 @@ __global__ __launch_bounds__(256, 2) void attn_gqa_kernel(DevPlan p, const __bf1
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[kb][r]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32)) * sl2;
+      mx = halves_max(mx) * sl2;
       // The reference max only moves when the tile's max exceeds it by more than 2^8, so most tiles
-      // skip rescaling the accumulators; probabilities stay below 256, which bf16/fp32 hold exactly
-      // as well as values below 1.  The final normalization uses the same reference, so the result
-      // does not depend on when it moved.
+      // skip rescaling the accumulators; probabilities stay below 256, which bf16/fp32 represent as
+      // well as values below 1.  The final normalization uses the same reference.
       const bool bump = mx > m_run + 8.0f;
       const float m_new = bump ? mx : m_run;
       const float m_use = (m_new == -INFINITY) ? 0.0f : m_new;
@@ -275,7 +270,7 @@ __global__ __launch_bounds__(256, 2) void attn_gqa_kernel(DevPlan p, const __bf1
           rs += e;
           pb[2 * kb + (r >> 3)][r & 7] = static_cast<__bf16>(e);
         }
-      rs += __shfl_xor(rs, 32);
+      rs = halves_sum(rs);
       if (__any(bump)) {
         const float alpha = fast_exp2(m_run - m_use);
         l_run *= alpha;
@@ -286,18 +281,18 @@ __global__ __launch_bounds__(256, 2) void attn_gqa_kernel(DevPlan p, const __bf1
       }
       l_run += rs;
       m_run = m_new;
-      // O^T[d][row] += V^T[d][key] P^T[key][row]; step t covers keys 16t + 8*(e/4) + 4*hf + (e%4)
+      // O^T[d][row] += V^T[d][key] P^T[key][row]; step t covers keys 16t + 8*(e/4) + 4*hf + (e%4),
+      // the order in which the S^T accumulator holds them
+      const __bf16* vl = &vs[buf][v_lane];
 #pragma unroll
-      for (int db = 0; db < D / 32; ++db) {
-        const __bf16* vrow = &vts[buf][(32 * db + col) * VSTR + 4 * hf];
+      for (int t = 0; t < 4; ++t)
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          const bf16x4 lo = *reinterpret_cast<const bf16x4*>(vrow + 16 * t);
-          const bf16x4 hi = *reinterpret_cast<const bf16x4*>(vrow + 16 * t + 8);
+        for (int db = 0; db < D / 32; ++db) {
+          const bf16x4 lo = lds_read_tr(vl + 16 * t * VSTR + 32 * db);
+          const bf16x4 hi = lds_read_tr(vl + (16 * t + 8) * VSTR + 32 * db);
           const bf16x8 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
           oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[t], oacc[db], 0, 0, 0);
         }
-      }
     }
     if (has_next) WAVEPP_STORE_TILE(buf ^ 1)
     __syncthreads();
@@ -306,7 +301,7 @@ __global__ __launch_bounds__(256, 2) void attn_gqa_kernel(DevPlan p, const __bf1
 #undef WAVEPP_LOAD_TILE
 #undef WAVEPP_STORE_TILE
 
-  // ---- epilogue: O = O^T / l, lse = ln(l) + m ---------------------------------------------------
+  // ---- epilogue: O = O^T / l, lse = ln(l) + m (natural log) ------------------------------------
   if (!row_ok) return;
   const float inv_l = l_run > 0.0f ? 1.0f / l_run : 0.0f;
   const float lse_v = l_run > 0.0f ? (m_run + __log2f(l_run)) * kLn2 : -INFINITY;

@@ -237,6 +237,14 @@ __global__ __launch_bounds__(256, 2) void attn_gqa_kernel(DevPlan p, const __bf1
           const bf16x8 kf = *reinterpret_cast<const bf16x8*>(kl + 32 * kb * KSTR + 16 * s);
           sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s], sacc[kb], 0, 0, 0);
         }
+      // keep four K fragment reads in flight ahead of the MFMAs that consume them
+      __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+      for (int i = 0; i < D / 8 - 4; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
       // accumulator element r of block kb holds key 32*kb + 8*(r/4) + 4*hf + (r%4)
       const bool need_mask = (kbase + KT - 1 > wave_min_lim) || (kbase + KT > it.kv_end);
       if (need_mask) {
@@ -293,6 +301,14 @@ __global__ __launch_bounds__(256, 2) void attn_gqa_kernel(DevPlan p, const __bf1
           const bf16x8 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
           oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[t], oacc[db], 0, 0, 0);
         }
+      // keep two MFMAs' worth of transposed V reads in flight
+      __builtin_amdgcn_sched_group_barrier(0x100, 4, 1);
+#pragma unroll
+      for (int i = 0; i < D / 8 - 2; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 1);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 1);
     }
     if (has_next) WAVEPP_STORE_TILE(buf ^ 1)
     __syncthreads();

@@ -109,11 +109,16 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run one plain device copy of this many MiB (HBM counter calibration)")
+    ap.add_argument("--measure-traffic", metavar="OUT_JSON", default=None,
+                    help="run rocprofv3 FETCH_SIZE and WRITE_SIZE passes over this config and write the per-launch "
+                         "HBM bytes of the attention kernel, calibrated against a plain copy, to OUT_JSON")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path (see DESIGN.md, sharding)",
+        print("bench.py measures one GPU only: the attention path has no multi-GPU implementation",
               file=sys.stderr)
         sys.exit(2)
+    if args.measure_traffic:
+        sys.exit(measure_traffic(args.config, args.measure_traffic))
 
     import numpy as np
     import torch
@@ -238,6 +243,50 @@ def main():
         fresh = cpu_layer0 if cpu_layer0 is not None else wl.make_tensors(spec, seed=seed, device=dev, poison=False)
         res["cpu_baseline"] = cpu_baseline(spec, fresh)
     print(json.dumps(res), flush=True)
+
+
+def measure_traffic(config, out_json, calib_mib=1024):
+    """Two rocprofv3 counter passes (FETCH_SIZE, then WRITE_SIZE) over a short run of this config.
+
+    Each counter is scaled by what it reads for one plain device copy of calib_mib MiB in the same
+    process (known bytes / counted bytes), then averaged over the attention launches.  The GPU is
+    not touched by this process itself: the profiled runs are child processes.
+    """
+    import csv
+    import subprocess
+    import tempfile
+    out = {"config": str(config), "kernel_source_hash": _kernel_hash(), "calibration_copy_mib": calib_mib}
+    known_kib = calib_mib * 1024.0
+    for counter in ("FETCH_SIZE", "WRITE_SIZE"):
+        d = tempfile.mkdtemp(prefix=f"wavepp_{counter.lower()}_", dir=os.environ.get("TMPDIR", "/tmp"))
+        cmd = ["rocprofv3", "--pmc", counter, "-f", "csv", "-d", d, "-o", "run", "--",
+               sys.executable, os.path.abspath(__file__), "--config", str(config), "--steps", "2", "--warmup", "1",
+               "--no-cpu-baseline", "--copy-calibration-mib", str(calib_mib)]
+        print("[traffic] " + " ".join(cmd), flush=True)
+        res = subprocess.run(cmd, cwd=os.environ.get("TMPDIR", "/tmp"), timeout=300)
+        rows = []
+        for root, _, files in os.walk(d):
+            for f in files:
+                if f.endswith("counter_collection.csv"):
+                    rows += list(csv.DictReader(open(os.path.join(root, f))))
+        if not rows:
+            print(f"[traffic] no counter rows (rc={res.returncode})", file=sys.stderr)
+            return 1
+        attn = [float(r["Counter_Value"]) for r in rows if "attn_" in r["Kernel_Name"]]
+        copy = [float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"]]
+        if not attn or not copy:
+            print("[traffic] attention or calibration copy kernel missing from the counter rows", file=sys.stderr)
+            return 1
+        factor = known_kib / copy[0]
+        out[counter] = {"kib_per_launch": sum(attn) / len(attn), "launches": len(attn),
+                        "calibration_kib": copy[0], "factor": factor,
+                        "bytes_per_launch": sum(attn) / len(attn) * factor * 1024.0}
+    out["bytes_per_launch"] = out["FETCH_SIZE"]["bytes_per_launch"] + out["WRITE_SIZE"]["bytes_per_launch"]
+    out["command"] = f"python bench.py --config {config} --measure-traffic {out_json}"
+    with open(out_json, "w") as f:
+        json.dump(out, f, indent=1)
+    print(json.dumps(out), flush=True)
+    return 0
 
 
 def _kernel_hash():

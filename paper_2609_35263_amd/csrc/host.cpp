@@ -69,7 +69,7 @@ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 bool supported_shape(const wavepp_attn_shape& s) {
   if (s.page_size != 16 && s.page_size != 64) return false;
-  if (s.kv_shared) return false;  // latent (576/512) kernel not built yet
+  if (s.kv_shared) return s.head_dim_qk == 576 && s.head_dim_v == 512 && s.num_kv_heads == 1;
   return (s.head_dim_qk == 64 && s.head_dim_v == 64) || (s.head_dim_qk == 128 && s.head_dim_v == 128);
 }
 

@@ -12,7 +12,7 @@ constexpr int kGqaRowsPerItem = 128;       // 4 waves x 32 query rows
 constexpr int kKvTile = 64;                // keys per inner-loop tile
 constexpr int kNumXcd = 8;                 // L2 domains a launch is spread over, round-robin
 constexpr int kMlaRowsPerItem = 64;        // latent kernel: query rows per work item
-constexpr int kMlaKvTile = 32;
+constexpr int kMlaKvTile = 64;             // latent kernel: keys per tile
 
 // Header at the start of the uploaded metadata.
 struct alignas(16) MetaHeader {

@@ -349,6 +349,266 @@ __global__ __launch_bounds__(256, 2) void attn_gqa_kernel(DevPlan p, const __bf1
 }
 
 // ---------------------------------------------------------------------------------------------
+// Latent attention in absorbed form: every query head attends over one shared 576-wide latent per
+// token (keys = the whole latent, values = its first 512 lanes).  Page size PAGE (16 or 64).
+//
+// One workgroup = 4 waves (one per SIMD) = 64 query rows; latent tiles of 64 keys.  Logits: wave w
+// computes S^T for key block w/2 (32 keys) and row block w%2 (32 rows), 36 MFMAs with its 32 Q rows
+// in registers; the two waves sharing a row block exchange their row maxima through LDS and apply
+// identical softmax decisions.  Values: wave w accumulates O for all 64 rows on value lanes
+// [128w, 128w + 128), so each latent element is read from LDS by one wave for the values and by two
+// for the keys.  The bf16 probabilities, already in MFMA B-operand order, pass through LDS.
+// ---------------------------------------------------------------------------------------------
+template <int PAGE>
+__global__ __launch_bounds__(256, 1) void attn_mla_kernel(DevPlan p, const __bf16* __restrict__ q,
+                                                          const __bf16* __restrict__ lat, __bf16* __restrict__ out,
+                                                          float* __restrict__ lse_out) {
+  constexpr int DQ = 576, DV = 512;
+  constexpr int KT = kMlaKvTile;        // 64 keys per tile
+  constexpr int STR = DQ + 8;           // latent rows in LDS (elements)
+  constexpr int CH = DQ / 8;            // 16-byte chunks per latent row
+  constexpr int LOADS = KT * CH / 256;  // chunks per thread per tile (18)
+  constexpr int ROUND = LOADS / 3;      // the next tile is staged in three rounds of registers
+  constexpr int PPT = (PAGE >= KT) ? 1 : KT / PAGE;
+  constexpr int DW = DV / 4;            // value lanes per wave
+  static_assert(LOADS * 256 == KT * CH && ROUND * 3 == LOADS, "tile covered exactly");
+  __shared__ __attribute__((aligned(16))) __bf16 lt[2][KT * STR];
+  __shared__ __attribute__((aligned(16))) bf16x8 pl[2][4][64];   // [row block][16-key step][lane]
+  __shared__ float xm[2][2][32];                                 // [key block][row block][row]: partial max
+  __shared__ int ovf;                                            // some row exceeded its softmax reference
+
+  if (!meta_ok(p)) return;
+  const WorkItem it = p.items[blockIdx.x];
+  if (it.rows <= 0) return;
+  const ReqMeta rm = p.reqs[it.req];
+  const int Hq = p.num_q_heads;
+  const int G = Hq;                     // a single latent head
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, col = lane & 31, hf = lane >> 5;
+  const int kb = wave >> 1, rb = wave & 1;
+  const int n_valid = rm.prefix + rm.chunk;
+  const int32_t* __restrict__ bt = p.bt + rm.bt_row;
+  const int64_t page_stride = int64_t(PAGE) * DQ;
+
+  // ---- this lane's S row -------------------------------------------------------------------------
+  const int lrow = rb * 32 + col;
+  const bool row_ok = lrow < it.rows;
+  const int prow = it.row0 + (row_ok ? lrow : 0);
+  const int tok = prow / G;
+  const int head = prow - tok * G;
+  const int limit = rm.prefix + tok;
+  bf16x8 qf[DQ / 16];
+  {
+    const __bf16* qrow = q + (int64_t(rm.cu + tok) * Hq + head) * DQ + 8 * hf;
+#pragma unroll
+    for (int s = 0; s < DQ / 16; ++s) qf[s] = row_ok ? *reinterpret_cast<const bf16x8*>(qrow + 16 * s) : bf16x8{};
+  }
+  const int blk_min_lim = rm.prefix + (it.row0 + 32 * rb) / G;
+
+  f32x16 oacc[2][DW / 32];              // [row block][value block]
+#pragma unroll
+  for (int r2 = 0; r2 < 2; ++r2)
+#pragma unroll
+    for (int db = 0; db < DW / 32; ++db) oacc[r2][db] = f32x16{};
+  float l_part = 0.0f;                  // this wave's key half of the row sum
+  const float sl2 = p.softmax_scale * kLog2e;
+
+  // ---- latent tile staging -----------------------------------------------------------------------
+  const int last_block = (n_valid - 1) / PAGE;
+  u32x4 sreg[ROUND];
+  int pg_nxt[PPT];
+#define WAVEPP_MLA_PAGES(tile_, pg_)                                                                      \
+  _Pragma("unroll") for (int i_ = 0; i_ < PPT; ++i_) pg_[i_] = bt[min((tile_) * (KT / PAGE) + i_, last_block)];
+#define WAVEPP_MLA_LOAD(tile_, pg_, i0_)                                                                  \
+  {                                                                                                       \
+    const int kbase_ = (tile_) * KT;                                                                      \
+    _Pragma("unroll") for (int i_ = 0; i_ < ROUND; ++i_) {                                                \
+      const int c_ = tid + 256 * ((i0_) + i_);                                                            \
+      const int j_ = min(kbase_ + c_ / CH, n_valid - 1);                                                  \
+      int page_ = pg_[0];                                                                                 \
+      _Pragma("unroll") for (int q_ = 1; q_ < PPT; ++q_) page_ = ((j_ - kbase_) / PAGE == q_) ? pg_[q_] : page_; \
+      sreg[i_] = *reinterpret_cast<const u32x4*>(lat + int64_t(page_) * page_stride +                     \
+                                                 (uint32_t(j_ % PAGE) * DQ + uint32_t(c_ % CH) * 8));     \
+    }                                                                                                     \
+  }
+#define WAVEPP_MLA_STORE(buf_, i0_)                                                                       \
+  _Pragma("unroll") for (int i_ = 0; i_ < ROUND; ++i_) {                                                  \
+    const int c_ = tid + 256 * ((i0_) + i_);                                                              \
+    *reinterpret_cast<u32x4*>(&lt[buf_][(c_ / CH) * STR + (c_ % CH) * 8]) = sreg[i_];                     \
+  }
+
+  const int k_lane = (32 * kb + col) * STR + 8 * hf;
+  const int v_lane = (4 * hf + (lane & 15) / 4) * STR + 16 * ((lane >> 4) & 1) + 4 * (lane & 3) + DW * wave;
+
+  const int t_begin = it.kv_begin / KT;
+  const int t_end = (it.kv_end + KT - 1) / KT;
+  // Softmax reference: fixed per row at its first visible tile and never moved within a pass, so the
+  // accumulators are never rescaled.  Later logits may exceed it by up to 2^64 in the exponent,
+  // which fp32 sums and bf16 probabilities hold for any realistic key count and value magnitude.  If
+  // a row ever exceeds that bound, the workgroup redoes its key range once with the exact row max
+  // (tracked during the first pass) as the reference, which no logit can exceed.
+  float m_ref = -INFINITY, m_true = -INFINITY;
+  for (int pass = 0; pass < 2; ++pass) {
+    if (tid == 0) ovf = 0;
+    {
+      int pg_cur[PPT];
+      WAVEPP_MLA_PAGES(t_begin, pg_cur)
+      WAVEPP_MLA_PAGES(t_begin + 1, pg_nxt)
+#pragma unroll
+      for (int rd = 0; rd < 3; ++rd) {
+        WAVEPP_MLA_LOAD(t_begin, pg_cur, rd * ROUND)
+        WAVEPP_MLA_STORE(0, rd * ROUND)
+      }
+    }
+    __syncthreads();
+
+    for (int tile = t_begin; tile < t_end; ++tile) {
+      const int buf = (tile - t_begin) & 1;
+      const bool has_next = tile + 1 < t_end;
+      if (has_next) WAVEPP_MLA_LOAD(tile + 1, pg_nxt, 0)
+      const int kbase = tile * KT + 32 * kb;
+      // S^T[key][row]: element r holds key kbase + 8*(r/4) + 4*hf + (r%4)
+      f32x16 sacc = f32x16{};
+      {
+        const __bf16* kl = &lt[buf][k_lane];
+#pragma unroll
+        for (int s = 0; s < DQ / 16; ++s) {
+          const bf16x8 kf = *reinterpret_cast<const bf16x8*>(kl + 16 * s);
+          sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s], sacc, 0, 0, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+        for (int i = 0; i < DQ / 16 - 4; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+      }
+      if ((kbase + 31 > blk_min_lim) || (kbase + 32 > it.kv_end)) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = kbase + 8 * (r >> 2) + 4 * hf + (r & 3);
+          if (key > limit || key >= it.kv_end) sacc[r] = -INFINITY;
+        }
+      }
+      float mx = -INFINITY;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[r]);
+      mx = halves_max(mx);
+      if (hf == 0) xm[kb][rb][col] = mx;
+      if (has_next) {
+        WAVEPP_MLA_STORE(buf ^ 1, 0)
+        WAVEPP_MLA_LOAD(tile + 1, pg_nxt, ROUND)
+      }
+      __syncthreads();
+      // both waves of a row block see the same maxima and make the same decisions
+      mx = fmaxf(xm[0][rb][col], xm[1][rb][col]) * sl2;
+      m_true = fmaxf(m_true, mx);
+      if (m_ref == -INFINITY) m_ref = mx;
+      if (mx > m_ref + 64.0f) ovf = 1;
+      const float m_use = (m_ref == -INFINITY) ? 0.0f : m_ref;
+      float ra = 0.0f, rz = 0.0f;
+      bf16x8 pb[2];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float e = fast_exp2(fmaf(sacc[r], sl2, -m_use));
+        if (r & 1) rz += e; else ra += e;
+        pb[r >> 3][r & 7] = static_cast<__bf16>(e);
+      }
+      l_part += halves_sum(ra + rz);
+      pl[rb][2 * kb][lane] = pb[0];
+      pl[rb][2 * kb + 1][lane] = pb[1];
+      if (has_next) {
+        WAVEPP_MLA_STORE(buf ^ 1, ROUND)
+        WAVEPP_MLA_LOAD(tile + 1, pg_nxt, 2 * ROUND)
+      }
+      __syncthreads();
+
+      // O^T[d][row] += V^T[d][key] P^T[key][row] on the wave's value lanes, for all 64 rows
+      {
+        const __bf16* vl = &lt[buf][v_lane];
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+          const bf16x8 p0 = pl[0][ks][lane];
+          const bf16x8 p1 = pl[1][ks][lane];
+#pragma unroll
+          for (int db = 0; db < DW / 32; ++db) {
+            const bf16x4 lo = lds_read_tr(vl + 16 * ks * STR + 32 * db);
+            const bf16x4 hi = lds_read_tr(vl + (16 * ks + 8) * STR + 32 * db);
+            const bf16x8 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+            oacc[0][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, p0, oacc[0][db], 0, 0, 0);
+            oacc[1][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, p1, oacc[1][db], 0, 0, 0);
+          }
+        }
+      }
+      if (has_next) {
+        WAVEPP_MLA_STORE(buf ^ 1, 2 * ROUND)
+        WAVEPP_MLA_PAGES(tile + 2, pg_nxt)
+      }
+      __syncthreads();
+    }
+    if (pass == 1 || ovf == 0) break;
+    // a reference was exceeded: start over with the exact row max
+    __syncthreads();
+    m_ref = m_true;
+    l_part = 0.0f;
+#pragma unroll
+    for (int r2 = 0; r2 < 2; ++r2)
+#pragma unroll
+      for (int db = 0; db < DW / 32; ++db) oacc[r2][db] = f32x16{};
+  }
+#undef WAVEPP_MLA_PAGES
+#undef WAVEPP_MLA_LOAD
+#undef WAVEPP_MLA_STORE
+
+  // ---- epilogue: row sum = both key halves; every wave normalizes its value lanes of all 64 rows ----
+  if (hf == 0) xm[kb][rb][col] = l_part;
+  __syncthreads();
+  if (kb == 0 && row_ok && hf == 0) {
+    const float l = xm[0][rb][col] + xm[1][rb][col];
+    const float m_use = (m_ref == -INFINITY) ? 0.0f : m_ref;
+    const float lse_v = l > 0.0f ? (m_use + __log2f(l)) * kLn2 : -INFINITY;
+    if (it.part < 0) {
+      if (lse_out) lse_out[int64_t(rm.cu + tok) * Hq + head] = lse_v;
+    } else {
+      p.lpart[it.part + lrow] = lse_v;
+    }
+  }
+#pragma unroll
+  for (int r2 = 0; r2 < 2; ++r2) {
+    const int r_local = 32 * r2 + col;
+    if (r_local >= it.rows) continue;
+    const float l = xm[0][r2][col] + xm[1][r2][col];
+    const float inv_l = l > 0.0f ? 1.0f / l : 0.0f;
+    const int pr = it.row0 + r_local;
+    const int tk = pr / G;
+    const int hd = pr - tk * G;
+    if (it.part < 0) {
+      __bf16* orow = out + (int64_t(rm.cu + tk) * Hq + hd) * DV + DW * wave;
+#pragma unroll
+      for (int db = 0; db < DW / 32; ++db)
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          bf16x4 v;
+#pragma unroll
+          for (int k = 0; k < 4; ++k) v[k] = static_cast<__bf16>(oacc[r2][db][4 * u + k] * inv_l);
+          *reinterpret_cast<bf16x4*>(orow + 32 * db + 8 * u + 4 * hf) = v;
+        }
+    } else {
+      float* orow = p.opart + int64_t(it.part + r_local) * DV + DW * wave;
+#pragma unroll
+      for (int db = 0; db < DW / 32; ++db)
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          f32x4 v;
+#pragma unroll
+          for (int k = 0; k < 4; ++k) v[k] = oacc[r2][db][4 * u + k] * inv_l;
+          *reinterpret_cast<f32x4*>(orow + 32 * db + 8 * u + 4 * hf) = v;
+        }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
 // Merge of key-range splits: o = sum_s w_s o_s / sum_s w_s with w_s = exp(lse_s - max lse),
 // lse = max + ln sum_s w_s.  Splits are combined in index order, so results are deterministic.
 // ---------------------------------------------------------------------------------------------
@@ -420,7 +680,16 @@ hipError_t launch_attention(const DevPlan& p, const void* q, const void* k_pool,
   auto vp = static_cast<const __bf16*>(v_pool);
   auto oo = static_cast<__bf16*>(out);
   const dim3 grid(p.num_items), block(256);
-  if (p.kv_shared) return hipErrorInvalidValue;
+  if (p.kv_shared) {
+    if (p.head_dim_qk != 576 || p.head_dim_v != 512) return hipErrorInvalidValue;
+    if (p.page_size == 64)
+      hipLaunchKernelGGL((attn_mla_kernel<64>), grid, block, 0, stream, p, qq, kp, oo, lse);
+    else if (p.page_size == 16)
+      hipLaunchKernelGGL((attn_mla_kernel<16>), grid, block, 0, stream, p, qq, kp, oo, lse);
+    else
+      return hipErrorInvalidValue;
+    return hipGetLastError();
+  }
   if (p.head_dim_qk == 128 && p.page_size == 64)
     hipLaunchKernelGGL((attn_gqa_kernel<128, 64>), grid, block, 0, stream, p, qq, kp, vp, oo, lse);
   else if (p.head_dim_qk == 128 && p.page_size == 16)

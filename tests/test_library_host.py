@@ -141,3 +141,22 @@ def test_plan_is_deterministic_and_independent_of_physical_pages():
     spec.block_table = perm[spec.block_table]
     c = wp.plan_for(spec).items()
     assert np.array_equal(a, c)
+
+
+def test_latent_plan_shapes():
+    ok = dict(num_q_heads=16, num_kv_heads=1, head_dim_qk=576, head_dim_v=512, page_size=64, num_pages=8,
+              softmax_scale=1 / 24, prefix_lens=[100], chunk_lens=[30], block_table=[[1, 4, 0]], kv_shared=True)
+    p = wp.plan(**ok)
+    info = p.info()
+    assert info["rows_per_item"] == 64 and info["kv_tile"] == 64 and info["num_real_items"] == 30 * 16 // 64 + 1
+    for over, status in [(dict(num_kv_heads=2, num_q_heads=16), -2), (dict(head_dim_v=576), -2),
+                         (dict(kv_shared=False), -2)]:
+        try:
+            wp.plan(**{**ok, **over})
+            got = 0
+        except wp.WaveppError as e:
+            got = e.status
+        assert got == status, (over, got)
+    spec = wl.custom_wave(16, 1, 576, 512, 16, [37, 200, 5], [20, 1, 90], kv_shared=True, seed=1)
+    for splits in (0, 2, 3):
+        coverage_check(spec, wp.plan_for(spec, max_splits=splits).items(), 64)

@@ -65,7 +65,7 @@ def load_library(path: str = None) -> ctypes.CDLL:
     global _lib
     if _lib is not None and path is None:
         return _lib
-    path = path or LIB_PATH
+    path = path or os.environ.get("WAVEPP_LIB") or LIB_PATH
     if not os.path.exists(path):
         raise RuntimeError(f"{path} is missing: build it first (python -m paper_2609_35263_amd.build)")
     lib = ctypes.CDLL(path)
@@ -90,8 +90,7 @@ def load_library(path: str = None) -> ctypes.CDLL:
     lib.wavepp_status_string.restype = ctypes.c_char_p
     lib.wavepp_last_error.argtypes = []
     lib.wavepp_last_error.restype = ctypes.c_char_p
-    if path == LIB_PATH:
-        _lib = lib
+    _lib = lib
     return lib
 
 

@@ -238,6 +238,7 @@ DevPlan make_dev(const wavepp_plan* plan, void* ws) {
   d.page_size = plan->shape.page_size;
   d.kv_shared = plan->shape.kv_shared;
   d.softmax_scale = plan->shape.softmax_scale;
+  d.rows_per_item = plan->rows_per_item;
   return d;
 }
 
@@ -328,7 +329,11 @@ int wavepp_attn_plan(const wavepp_attn_shape* shape, const wavepp_batch* batch, 
   plan->total_tokens = total;
   plan->serial = g_serial.fetch_add(1);
   const bool mla = s.kv_shared != 0;
-  const int M = mla ? kMlaRowsPerItem : kGqaRowsPerItem;
+  // grouped kernel: 8 waves (256 rows) per workgroup, one workgroup per CU: each K/V tile staged in
+  // LDS serves twice the rows of the 4-wave layout (WAVEPP_GQA_WAVES=4), halving K/V traffic per row
+  const char* gw = getenv("WAVEPP_GQA_WAVES");
+  const int gqa_rows = (gw && atoi(gw) == 4) ? kGqaRowsPerItem / 2 : kGqaRowsPerItem;
+  const int M = mla ? kMlaRowsPerItem : gqa_rows;
   const int KT = mla ? kMlaKvTile : kKvTile;
   plan->rows_per_item = M;
   plan->kv_tile = KT;

@@ -8,7 +8,7 @@
 namespace wavepp {
 
 constexpr uint32_t kMagic = 0x57415650u;   // "WAVP"
-constexpr int kGqaRowsPerItem = 128;       // 4 waves x 32 query rows
+constexpr int kGqaRowsPerItem = 256;       // grouped kernel: 8 waves x 32 query rows
 constexpr int kKvTile = 64;                // keys per inner-loop tile
 constexpr int kNumXcd = 8;                 // L2 domains a launch is spread over, round-robin
 constexpr int kMlaRowsPerItem = 64;        // latent kernel: query rows per work item
@@ -71,6 +71,7 @@ struct DevPlan {
   int32_t num_merge;
   int64_t total_tokens;
   int32_t num_q_heads, num_kv_heads, head_dim_qk, head_dim_v, page_size, kv_shared;
+  int32_t rows_per_item;   // query rows per attention workgroup (32 per wave)
   float softmax_scale;
 };
 

@@ -1,7 +1,8 @@
 // gfx950 (CDNA4) kernels of libwavepp_attn: K/V append into reserved pages, chunked-prefill
 // attention over paged K/V with bf16 MFMA, and the merge of key-range splits.
 //
-// Attention layout (one workgroup = 4 waves = one work item of up to 128 query rows):
+// Attention layout (one workgroup = 8 waves = one work item of up to 256 query rows; one workgroup
+// per CU, two waves per SIMD):
 //   * Rows are (token, head-in-group) pairs of one (request, KV head): row = token * G + h, so the
 //     G query heads that share a KV head share every K/V tile loaded into LDS.
 //   * Each wave owns 32 rows.  Logits are computed transposed, S^T = K Q^T, with
@@ -105,18 +106,19 @@ __device__ __forceinline__ bf16x4 lds_read_tr(const __bf16* p) {
   return __builtin_bit_cast(bf16x4, r);
 }
 
-template <int D, int PAGE>
-__global__ __launch_bounds__(256, 2) void attn_gqa_kernel(DevPlan p, const __bf16* __restrict__ q,
+template <int D, int PAGE, int NW>
+__global__ __launch_bounds__(NW * 64) void attn_gqa_kernel(DevPlan p, const __bf16* __restrict__ q,
                                                           const __bf16* __restrict__ kpool,
                                                           const __bf16* __restrict__ vpool, __bf16* __restrict__ out,
                                                           float* __restrict__ lse_out) {
   constexpr int KT = kKvTile;          // 64 keys per tile
+  constexpr int NT = NW * 64;          // threads per workgroup; NW waves x 32 query rows
   constexpr int KSTR = D + 8;          // K rows in LDS: 16-byte reads of 8 rows land on distinct banks
   constexpr int VSTR = D + 16;         // V rows in LDS: transposed reads of 4 rows x 32 bytes on distinct banks
   constexpr int CH = D / 8;            // 16-byte chunks per key row
-  constexpr int LOADS = KT * CH / 256; // chunks per thread per tile, for K and for V alike
+  constexpr int LOADS = KT * CH / NT;  // chunks per thread per tile, for K and for V alike
   constexpr int PPT = (PAGE >= KT) ? 1 : KT / PAGE;   // pages touched by one tile
-  static_assert(LOADS * 256 == KT * CH, "tile covered exactly");
+  static_assert(LOADS >= 1 && LOADS * NT == KT * CH, "tile covered exactly");
   __shared__ __attribute__((aligned(16))) __bf16 ks[2][KT * KSTR];
   __shared__ __attribute__((aligned(16))) __bf16 vs[2][KT * VSTR];
 
@@ -159,20 +161,23 @@ __global__ __launch_bounds__(256, 2) void attn_gqa_kernel(DevPlan p, const __bf1
   const float sl2 = p.softmax_scale * kLog2e;
 
   // ---- K/V tile staging -----------------------------------------------------------------------
-  // Thread tid moves 16-byte chunks c = tid + 256 i of both the K and the V tile: key c / CH, chunk
+  // Thread tid moves 16-byte chunks c = tid + NT i of both the K and the V tile: key c / CH, chunk
   // c % CH; consecutive threads read consecutive 16 bytes of a page's contiguous head slice.  The
   // physical pages of a tile are looked up one tile ahead (uniform across the workgroup, hence
-  // scalar loads) and the loads of tile t+1 are issued before the MFMAs of tile t.  In the last
-  // tile of a request, key positions past its last valid slot are clamped to that slot: those rows
-  // are finite copies that the mask gives zero weight, so stale or NaN pool slots are never read.
+  // scalar loads) and the loads of tile t+1 are issued before the MFMAs of tile t.  A whole tile
+  // uses offsets fixed per thread; in the last tile of a request, key positions past its last valid
+  // slot are clamped to that slot: those rows are finite copies that the mask gives zero weight, so
+  // stale or NaN pool slots are never read.
   const int last_block = (n_valid - 1) / PAGE;
-  int ckey[LOADS];
-  uint32_t coff[LOADS];
+  int ckey[LOADS], csub[LOADS];
+  uint32_t coff[LOADS], cfull[LOADS];
 #pragma unroll
   for (int i = 0; i < LOADS; ++i) {
-    const int c = tid + 256 * i;
+    const int c = tid + NT * i;
     ckey[i] = c / CH;
+    csub[i] = ckey[i] / PAGE;
     coff[i] = uint32_t((c % CH) * 8);
+    cfull[i] = uint32_t(ckey[i] % PAGE) * D + coff[i];
   }
   u32x4 kreg[LOADS], vreg[LOADS];
   int pg_nxt[PPT];
@@ -183,15 +188,23 @@ __global__ __launch_bounds__(256, 2) void attn_gqa_kernel(DevPlan p, const __bf1
 #define WAVEPP_LOAD_TILE(tile_, pg_)                                                                      \
   {                                                                                                       \
     const int kbase_ = (tile_) * KT;                                                                      \
-    const bool full_ = kbase_ + KT <= n_valid;                                                            \
-    _Pragma("unroll") for (int i_ = 0; i_ < LOADS; ++i_) {                                                \
-      const int j_ = full_ ? kbase_ + ckey[i_] : min(kbase_ + ckey[i_], n_valid - 1);                     \
-      const int sub_ = (j_ - kbase_) / PAGE;                                                              \
-      int page_ = pg_[0];                                                                                 \
-      _Pragma("unroll") for (int q_ = 1; q_ < PPT; ++q_) page_ = (sub_ == q_) ? pg_[q_] : page_;          \
-      const uint32_t off_ = uint32_t(j_ % PAGE) * D + coff[i_];                                           \
-      kreg[i_] = *reinterpret_cast<const u32x4*>(kpool_h + int64_t(page_) * page_stride + off_);         \
-      vreg[i_] = *reinterpret_cast<const u32x4*>(vpool_h + int64_t(page_) * page_stride + off_);         \
+    if (kbase_ + KT <= n_valid) {                                                                         \
+      _Pragma("unroll") for (int i_ = 0; i_ < LOADS; ++i_) {                                              \
+        int page_ = pg_[0];                                                                               \
+        _Pragma("unroll") for (int q_ = 1; q_ < PPT; ++q_) page_ = (csub[i_] == q_) ? pg_[q_] : page_;    \
+        kreg[i_] = *reinterpret_cast<const u32x4*>(kpool_h + int64_t(page_) * page_stride + cfull[i_]);   \
+        vreg[i_] = *reinterpret_cast<const u32x4*>(vpool_h + int64_t(page_) * page_stride + cfull[i_]);   \
+      }                                                                                                   \
+    } else {                                                                                              \
+      _Pragma("unroll") for (int i_ = 0; i_ < LOADS; ++i_) {                                              \
+        const int j_ = min(kbase_ + ckey[i_], n_valid - 1);                                               \
+        const int sub_ = (j_ - kbase_) / PAGE;                                                            \
+        int page_ = pg_[0];                                                                               \
+        _Pragma("unroll") for (int q_ = 1; q_ < PPT; ++q_) page_ = (sub_ == q_) ? pg_[q_] : page_;        \
+        const uint32_t off_ = uint32_t(j_ % PAGE) * D + coff[i_];                                         \
+        kreg[i_] = *reinterpret_cast<const u32x4*>(kpool_h + int64_t(page_) * page_stride + off_);       \
+        vreg[i_] = *reinterpret_cast<const u32x4*>(vpool_h + int64_t(page_) * page_stride + off_);       \
+      }                                                                                                   \
     }                                                                                                     \
   }
 
@@ -690,16 +703,24 @@ hipError_t launch_attention(const DevPlan& p, const void* q, const void* k_pool,
       return hipErrorInvalidValue;
     return hipGetLastError();
   }
-  if (p.head_dim_qk == 128 && p.page_size == 64)
-    hipLaunchKernelGGL((attn_gqa_kernel<128, 64>), grid, block, 0, stream, p, qq, kp, vp, oo, lse);
-  else if (p.head_dim_qk == 128 && p.page_size == 16)
-    hipLaunchKernelGGL((attn_gqa_kernel<128, 16>), grid, block, 0, stream, p, qq, kp, vp, oo, lse);
-  else if (p.head_dim_qk == 64 && p.page_size == 64)
-    hipLaunchKernelGGL((attn_gqa_kernel<64, 64>), grid, block, 0, stream, p, qq, kp, vp, oo, lse);
-  else if (p.head_dim_qk == 64 && p.page_size == 16)
-    hipLaunchKernelGGL((attn_gqa_kernel<64, 16>), grid, block, 0, stream, p, qq, kp, vp, oo, lse);
-  else
+  const bool w8 = p.rows_per_item == 256;
+  if (!w8 && p.rows_per_item != 128) return hipErrorInvalidValue;
+  const dim3 block_g(w8 ? 512 : 256);
+#define WAVEPP_GQA(D_, P_)                                                                                 \
+  if (w8) hipLaunchKernelGGL((attn_gqa_kernel<D_, P_, 8>), grid, block_g, 0, stream, p, qq, kp, vp, oo, lse); \
+  else hipLaunchKernelGGL((attn_gqa_kernel<D_, P_, 4>), grid, block_g, 0, stream, p, qq, kp, vp, oo, lse);
+  if (p.head_dim_qk == 128 && p.page_size == 64) {
+    WAVEPP_GQA(128, 64)
+  } else if (p.head_dim_qk == 128 && p.page_size == 16) {
+    WAVEPP_GQA(128, 16)
+  } else if (p.head_dim_qk == 64 && p.page_size == 64) {
+    WAVEPP_GQA(64, 64)
+  } else if (p.head_dim_qk == 64 && p.page_size == 16) {
+    WAVEPP_GQA(64, 16)
+  } else {
     return hipErrorInvalidValue;
+  }
+#undef WAVEPP_GQA
   return hipGetLastError();
 }
 

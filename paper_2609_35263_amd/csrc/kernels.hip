@@ -111,10 +111,11 @@ __global__ __launch_bounds__(NW * 64) void attn_gqa_kernel(DevPlan p, const __bf
                                                           const __bf16* __restrict__ kpool,
                                                           const __bf16* __restrict__ vpool, __bf16* __restrict__ out,
                                                           float* __restrict__ lse_out) {
-  constexpr int KT = kKvTile;          // 64 keys per tile
+  constexpr int KT = kKvTile;          // keys per tile
+  constexpr int NKB = KT / 32;         // 32-key blocks per tile
   constexpr int NT = NW * 64;          // threads per workgroup; NW waves x 32 query rows
   constexpr int KSTR = D + 8;          // K rows in LDS: 16-byte reads of 8 rows land on distinct banks
-  constexpr int VSTR = D + 16;         // V rows in LDS: transposed reads of 4 rows x 32 bytes on distinct banks
+  constexpr int VSTR = D + 32;         // V rows in LDS: transposed reads of 4 rows x 2 groups x 32 bytes on distinct banks
   constexpr int CH = D / 8;            // 16-byte chunks per key row
   constexpr int LOADS = KT * CH / NT;  // chunks per thread per tile, for K and for V alike
   constexpr int PPT = (PAGE >= KT) ? 1 : KT / PAGE;   // pages touched by one tile
@@ -240,20 +241,22 @@ __global__ __launch_bounds__(NW * 64) void attn_gqa_kernel(DevPlan p, const __bf
     }
     const int kbase = tile * KT;
     if (wave_active && kbase <= wave_max_lim) {
-      // S^T[key][row] for the 64 keys of the tile, as two 32-key blocks
-      f32x16 sacc[2] = {f32x16{}, f32x16{}};
+      // S^T[key][row] for the KT keys of the tile, as NKB 32-key blocks
+      f32x16 sacc[NKB];
+#pragma unroll
+      for (int kb = 0; kb < NKB; ++kb) sacc[kb] = f32x16{};
       const __bf16* kl = &ks[buf][k_lane];
 #pragma unroll
       for (int s = 0; s < D / 16; ++s)
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
+        for (int kb = 0; kb < NKB; ++kb) {
           const bf16x8 kf = *reinterpret_cast<const bf16x8*>(kl + 32 * kb * KSTR + 16 * s);
           sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s], sacc[kb], 0, 0, 0);
         }
       // keep four K fragment reads in flight ahead of the MFMAs that consume them
       __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
 #pragma unroll
-      for (int i = 0; i < D / 8 - 4; ++i) {
+      for (int i = 0; i < (D / 16) * NKB - 4; ++i) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
         __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
       }
@@ -262,7 +265,7 @@ __global__ __launch_bounds__(NW * 64) void attn_gqa_kernel(DevPlan p, const __bf
       const bool need_mask = (kbase + KT - 1 > wave_min_lim) || (kbase + KT > it.kv_end);
       if (need_mask) {
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+        for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const int key = kbase + 32 * kb + 8 * (r >> 2) + 4 * hf + (r & 3);
@@ -271,7 +274,7 @@ __global__ __launch_bounds__(NW * 64) void attn_gqa_kernel(DevPlan p, const __bf
       }
       float mx = -INFINITY;
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+      for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[kb][r]);
       mx = halves_max(mx) * sl2;
@@ -282,9 +285,9 @@ __global__ __launch_bounds__(NW * 64) void attn_gqa_kernel(DevPlan p, const __bf
       const float m_new = bump ? mx : m_run;
       const float m_use = (m_new == -INFINITY) ? 0.0f : m_new;
       float rs = 0.0f;
-      bf16x8 pb[4];
+      bf16x8 pb[2 * NKB];
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+      for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const float e = fast_exp2(fmaf(sacc[kb][r], sl2, -m_use));
@@ -306,7 +309,7 @@ __global__ __launch_bounds__(NW * 64) void attn_gqa_kernel(DevPlan p, const __bf
       // the order in which the S^T accumulator holds them
       const __bf16* vl = &vs[buf][v_lane];
 #pragma unroll
-      for (int t = 0; t < 4; ++t)
+      for (int t = 0; t < 2 * NKB; ++t)
 #pragma unroll
         for (int db = 0; db < D / 32; ++db) {
           const bf16x4 lo = lds_read_tr(vl + 16 * t * VSTR + 32 * db);
@@ -317,7 +320,7 @@ __global__ __launch_bounds__(NW * 64) void attn_gqa_kernel(DevPlan p, const __bf
       // keep two MFMAs' worth of transposed V reads in flight
       __builtin_amdgcn_sched_group_barrier(0x100, 4, 1);
 #pragma unroll
-      for (int i = 0; i < D / 8 - 2; ++i) {
+      for (int i = 0; i < (D / 32) * 2 * NKB - 2; ++i) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
         __builtin_amdgcn_sched_group_barrier(0x100, 2, 1);
       }

@@ -164,10 +164,10 @@ def test_single_visible_key_is_bit_exact():
 def test_wrong_workspace_or_small_workspace():
     torch = _torch()
     import paper_2609_35263_amd as wp
-    spec = wl.cfg1()
+    spec = wl.custom_wave(8, 2, 64, 64, 16, [500], [32], seed=3)
     t = wl.make_tensors(spec, seed=1000)
     p = wp.plan_for(spec, max_splits=2)
-    assert p.workspace_bytes > 256
+    assert p.workspace_bytes > 256                  # split partials need workspace beyond the metadata
     small = torch.empty(p.workspace_bytes - 256, dtype=torch.uint8, device="cuda")
     with pytest.raises(wp.WaveppError) as e:
         wp.plan_upload(p, small)

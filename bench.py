@@ -21,6 +21,7 @@ if ROOT not in sys.path:
 
 PEAK_BF16_TFLOPS = 2516.6     # 256 CU x 2.4 GHz x 4096 dense bf16 FLOP/clk/CU
 PEAK_HBM_GBS = 8000.0
+RIDGE_FLOP_PER_BYTE = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)     # ~315 FLOP/B
 METRIC = "chunked-prefill attention TFLOP/s + new tokens/s on 1 GPU; % of bf16 MFMA peak"
 
 
@@ -207,6 +208,17 @@ def main():
                 traffic = tj.get("bytes_per_launch")
         except Exception:
             traffic = None
+    b_layer = bytes_alg(spec)
+    kernel_name = "attn_gqa_kernel" if not spec.kv_shared else "attn_mla_kernel"
+    if f_layer / b_layer >= RIDGE_FLOP_PER_BYTE:
+        roofline = {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                    "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic, "kernel": kernel_name,
+                    "alg_flop_per_launch": f_layer, "alg_bytes_per_launch": b_layer}
+    else:
+        gbps = b_layer / (attn_ms * 1e-3) / 1e9
+        roofline = {"bound": "hbm", "achieved": round(gbps, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                    "frac": round(gbps / PEAK_HBM_GBS, 4), "traffic": traffic, "kernel": kernel_name,
+                    "alg_flop_per_launch": f_layer, "alg_bytes_per_launch": b_layer}
     res = {
         "metric": METRIC,
         "value": round(value, 3),
@@ -232,11 +244,9 @@ def main():
         "attn_kernel_ms": round(attn_ms, 4),
         "append_ms": round(append_ms, 4),
         "append_GBps": round(append_bytes(spec) / (append_ms * 1e-3) / 1e9, 1),
+        "attn_alg_GBps": round(bytes_alg(spec) / (attn_ms * 1e-3) / 1e9, 1),
         "work_items": info["num_items"],
-        "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic,
-                     "kernel": "attn_gqa_kernel" if not spec.kv_shared else "attn_mla_kernel",
-                     "alg_flop_per_launch": f_layer, "alg_bytes_per_launch": bytes_alg(spec)},
+        "roofline": roofline,
     }
     if not args.no_cpu_baseline:
         # the pools were appended to in place on the device; start from the generator's output again

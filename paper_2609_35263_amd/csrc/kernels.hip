@@ -630,38 +630,40 @@ __global__ __launch_bounds__(256, 1) void attn_mla_kernel(DevPlan p, const __bf1
 // ---------------------------------------------------------------------------------------------
 template <int DV>
 __global__ __launch_bounds__(256) void merge_kernel(DevPlan p, __bf16* __restrict__ out, float* __restrict__ lse_out) {
+  // workgroup (x = merge item, y = row group) handles RPB rows; one thread per (row, 4 value lanes)
+  constexpr int C4 = DV / 4;
+  constexpr int RPB = 256 / C4;
   if (!meta_ok(p)) return;
   const MergeItem mi = p.merges[blockIdx.x];
+  const int lrow = blockIdx.y * RPB + threadIdx.x / C4;
+  const int c4 = threadIdx.x % C4;
+  if (lrow >= mi.rows) return;
   const ReqMeta rm = p.reqs[mi.req];
   const int Hq = p.num_q_heads, G = Hq / p.num_kv_heads;
-  constexpr int C4 = DV / 4;
-  for (int idx = threadIdx.x; idx < mi.rows * C4; idx += blockDim.x) {
-    const int lrow = idx / C4, c4 = idx - lrow * C4;
-    float mx = -INFINITY;
-    for (int s = 0; s < mi.nsplit; ++s) mx = fmaxf(mx, p.lpart[mi.part + s * mi.rows + lrow]);
-    f32x4 acc = f32x4{};
-    float wsum = 0.0f;
-    for (int s = 0; s < mi.nsplit; ++s) {
-      const int prow = mi.part + s * mi.rows + lrow;
-      const float l = p.lpart[prow];
-      const float w = (l == -INFINITY) ? 0.0f : fast_exp2((l - mx) * kLog2e);
-      if (w != 0.0f) {
-        const f32x4 v = *reinterpret_cast<const f32x4*>(p.opart + int64_t(prow) * DV + 4 * c4);
-        acc += w * v;
-      }
-      wsum += w;
+  float mx = -INFINITY;
+  for (int s = 0; s < mi.nsplit; ++s) mx = fmaxf(mx, p.lpart[mi.part + s * mi.rows + lrow]);
+  f32x4 acc = f32x4{};
+  float wsum = 0.0f;
+  for (int s = 0; s < mi.nsplit; ++s) {
+    const int prow = mi.part + s * mi.rows + lrow;
+    const float l = p.lpart[prow];
+    const float w = (l == -INFINITY) ? 0.0f : fast_exp2((l - mx) * kLog2e);
+    if (w != 0.0f) {
+      const f32x4 v = *reinterpret_cast<const f32x4*>(p.opart + int64_t(prow) * DV + 4 * c4);
+      acc += w * v;
     }
-    const float inv = 1.0f / wsum;
-    const int row = mi.row0 + lrow;
-    const int tok = row / G;
-    const int head = mi.kv_head * G + (row - tok * G);
-    bf16x4 o;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) o[k] = static_cast<__bf16>(acc[k] * inv);
-    const int64_t orow = int64_t(rm.cu + tok) * Hq + head;
-    *reinterpret_cast<bf16x4*>(out + orow * DV + 4 * c4) = o;
-    if (lse_out && c4 == 0) lse_out[orow] = mx + __logf(wsum);
+    wsum += w;
   }
+  const float inv = 1.0f / wsum;
+  const int row = mi.row0 + lrow;
+  const int tok = row / G;
+  const int head = mi.kv_head * G + (row - tok * G);
+  bf16x4 o;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) o[k] = static_cast<__bf16>(acc[k] * inv);
+  const int64_t orow = int64_t(rm.cu + tok) * Hq + head;
+  *reinterpret_cast<bf16x4*>(out + orow * DV + 4 * c4) = o;
+  if (lse_out && c4 == 0) lse_out[orow] = mx + __logf(wsum);
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -730,7 +732,9 @@ hipError_t launch_attention(const DevPlan& p, const void* q, const void* k_pool,
 hipError_t launch_merge(const DevPlan& p, void* out, float* lse, hipStream_t stream) {
   if (p.num_merge == 0) return hipSuccess;
   auto oo = static_cast<__bf16*>(out);
-  const dim3 grid(p.num_merge), block(256);
+  const int c4 = p.head_dim_v / 4;
+  const int rpb = 256 / c4;
+  const dim3 grid(p.num_merge, (p.rows_per_item + rpb - 1) / rpb), block(256);
   if (p.head_dim_v == 128)
     hipLaunchKernelGGL((merge_kernel<128>), grid, block, 0, stream, p, oo, lse);
   else if (p.head_dim_v == 64)

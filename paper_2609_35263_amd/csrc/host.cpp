@@ -329,10 +329,17 @@ int wavepp_attn_plan(const wavepp_attn_shape* shape, const wavepp_batch* batch, 
   plan->total_tokens = total;
   plan->serial = g_serial.fetch_add(1);
   const bool mla = s.kv_shared != 0;
-  // grouped kernel: 8 waves (256 rows) per workgroup, one workgroup per CU: each K/V tile staged in
-  // LDS serves twice the rows of the 4-wave layout (WAVEPP_GQA_WAVES=4), halving K/V traffic per row
+  // grouped kernel: 8 waves (256 rows) per workgroup and one workgroup per CU, so that each K/V tile
+  // staged in LDS serves 256 rows.  When no (request, KV head) has more than 128 rows (short
+  // chunks: the wave is bound by streaming the prefix K/V), half of those waves would idle: the
+  // plan then uses 128-row items, run by the 4-wave form of the kernel, two workgroups per CU.
+  // WAVEPP_GQA_WAVES=4 or 8 forces one form.
+  int64_t max_rows = 0;
+  for (int32_t r = 0; r < R; ++r) max_rows = std::max<int64_t>(max_rows, int64_t(batch->chunk_lens[r]) * (s.num_q_heads / s.num_kv_heads));
   const char* gw = getenv("WAVEPP_GQA_WAVES");
-  const int gqa_rows = (gw && atoi(gw) == 4) ? kGqaRowsPerItem / 2 : kGqaRowsPerItem;
+  const int gw_n = gw ? atoi(gw) : 0;
+  const bool small_rows = gw_n == 4 || (gw_n != 8 && max_rows <= kGqaRowsPerItem / 2);
+  const int gqa_rows = small_rows ? kGqaRowsPerItem / 2 : kGqaRowsPerItem;
   const int M = mla ? kMlaRowsPerItem : gqa_rows;
   const int KT = mla ? kMlaKvTile : kKvTile;
   plan->rows_per_item = M;

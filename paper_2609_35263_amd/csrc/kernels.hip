@@ -107,11 +107,11 @@ __device__ __forceinline__ bf16x4 lds_read_tr(const __bf16* p) {
 }
 
 template <int D, int PAGE, int NW>
-__global__ __launch_bounds__(NW * 64) void attn_gqa_kernel(DevPlan p, const __bf16* __restrict__ q,
+__global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_gqa_kernel(DevPlan p, const __bf16* __restrict__ q,
                                                           const __bf16* __restrict__ kpool,
                                                           const __bf16* __restrict__ vpool, __bf16* __restrict__ out,
                                                           float* __restrict__ lse_out) {
-  constexpr int KT = kKvTile;          // keys per tile
+  constexpr int KT = NW == 4 ? kKvTile / 2 : kKvTile;   // keys per tile (4-wave form: two workgroups per CU)
   constexpr int NKB = KT / 32;         // 32-key blocks per tile
   constexpr int NT = NW * 64;          // threads per workgroup; NW waves x 32 query rows
   constexpr int KSTR = D + 8;          // K rows in LDS: 16-byte reads of 8 rows land on distinct banks

@@ -264,13 +264,13 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_gqa_kernel(DevP
       // accumulator element r of block kb holds key 32*kb + 8*(r/4) + 4*hf + (r%4)
       const bool need_mask = (kbase + KT - 1 > wave_min_lim) || (kbase + KT > it.kv_end);
       if (need_mask) {
+        // key > limit or key >= kv_end  <=>  (key - kbase - 4 hf) > bound, one compare per element
+        const int bound = min(limit, it.kv_end - 1) - kbase - 4 * hf;
 #pragma unroll
         for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int key = kbase + 32 * kb + 8 * (r >> 2) + 4 * hf + (r & 3);
-            if (key > limit || key >= it.kv_end) sacc[kb][r] = -INFINITY;
-          }
+          for (int r = 0; r < 16; ++r)
+            if (32 * kb + 8 * (r >> 2) + (r & 3) > bound) sacc[kb][r] = -INFINITY;
       }
       float mx = -INFINITY;
 #pragma unroll
@@ -500,11 +500,11 @@ __global__ __launch_bounds__(256, 1) void attn_mla_kernel(DevPlan p, const __bf1
         __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
       }
       if ((kbase + 31 > blk_min_lim) || (kbase + 32 > it.kv_end)) {
+        // key > limit or key >= kv_end  <=>  (key - kbase - 4 hf) > bound, one compare per element
+        const int bound = min(limit, it.kv_end - 1) - kbase - 4 * hf;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = kbase + 8 * (r >> 2) + 4 * hf + (r & 3);
-          if (key > limit || key >= it.kv_end) sacc[r] = -INFINITY;
-        }
+        for (int r = 0; r < 16; ++r)
+          if (8 * (r >> 2) + (r & 3) > bound) sacc[r] = -INFINITY;
       }
       float mx = -INFINITY;
 #pragma unroll

@@ -50,6 +50,12 @@ def test_cfg2_full():
     check_wave(wl.cfg2(), seed=2000)
 
 
+def test_cfg2_full_four_wave_form(monkeypatch):
+    """The 4-wave kernel form (128-row items, 64-key tiles, two workgroups per CU) on the whole cfg2 wave."""
+    monkeypatch.setenv("WAVEPP_GQA_WAVES", "4")
+    check_wave(wl.cfg2(), seed=2001)
+
+
 @pytest.mark.parametrize("case", [
     # Hq, Hkv, d, B, prefix, chunk
     (8, 2, 128, 16, [48, 0, 130], [32, 7, 61]),       # d=128 on 16-token pages, p = 0, mid-page start
@@ -189,6 +195,11 @@ def test_sampled_rows_cfg3():
 
 def test_sampled_rows_cfg4_layer():
     sampled_config_check(wl.cfg4(), seed=4000)
+
+
+def test_sampled_rows_small_chunk_wave():
+    """16-token chunks over 16K-32K cached tokens: 128-row items, automatic key-range splits and the merge."""
+    sampled_config_check(wl.small_chunk(16), seed=7016)
 
 
 def sampled_config_check(spec, seed, rows_per_req=16, max_requests=None):

@@ -132,6 +132,26 @@ def test_work_list_cfg2_and_auto_splits():
     coverage_check(small, ps.items(), 64)
 
 
+def test_item_rows_follow_the_largest_chunk(monkeypatch):
+    """128-row items (4-wave kernel form, two workgroups per CU) exactly when no (request, KV head)
+    has more than 128 rows; WAVEPP_GQA_WAVES forces either form."""
+    monkeypatch.delenv("WAVEPP_GQA_WAVES", raising=False)
+    assert wp.plan_for(wl.small_chunk(16)).info()["rows_per_item"] == 128      # 16 tokens x G 8
+    assert wp.plan_for(wl.small_chunk(32)).info()["rows_per_item"] == 256      # 32 x 8 = 256 rows
+    assert wp.plan_for(wl.cfg1()).info()["rows_per_item"] == 128               # 32 x 4
+    assert wp.plan_for(wl.cfg2()).info()["rows_per_item"] == 256
+    edge = wl.custom_wave(16, 2, 64, 64, 16, [40, 3], [16, 15], seed=2)        # 16 x 8 = 128 rows: small
+    assert wp.plan_for(edge).info()["rows_per_item"] == 128
+    edge = wl.custom_wave(16, 2, 64, 64, 16, [40, 3], [17, 15], seed=2)        # 17 x 8 = 136 rows
+    assert wp.plan_for(edge).info()["rows_per_item"] == 256
+    monkeypatch.setenv("WAVEPP_GQA_WAVES", "8")
+    assert wp.plan_for(wl.small_chunk(16)).info()["rows_per_item"] == 256
+    monkeypatch.setenv("WAVEPP_GQA_WAVES", "4")
+    p = wp.plan_for(wl.cfg2())
+    assert p.info()["rows_per_item"] == 128
+    coverage_check(wl.cfg2(), p.items(), p.info()["kv_tile"])
+
+
 def test_plan_is_deterministic_and_independent_of_physical_pages():
     spec = wl.cfg2()
     a = wp.plan_for(spec).items()

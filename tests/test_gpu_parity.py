@@ -157,6 +157,18 @@ def test_needles_through_permuted_pages():
     _compare.assert_parity(out_f64(g["out"]), ref["o"], g["lse"].cpu().numpy(), ref["lse"], "needles")
 
 
+def test_idle_wave_is_a_no_op():
+    """A wave whose requests all have empty chunks (c_r = 0): every entry point returns OK and the
+    pools are left as they were."""
+    spec = wl.custom_wave(8, 2, 64, 64, 16, [48, 0, 130], [0, 0, 0], seed=3)
+    t = wl.make_tensors(spec, seed=3, poison=True)
+    before = {k: wl.to_bits(t[k]) for k in ("k_pool", "v_pool")}
+    g = gpu_wave(spec, t)
+    assert g["plan"].info()["num_items"] == 0 and g["out"].shape[0] == 0
+    for k in ("k_pool", "v_pool"):
+        assert np.array_equal(wl.to_bits(g[k]), before[k]), k
+
+
 def test_single_visible_key_is_bit_exact():
     torch = _torch()
     spec = wl.custom_wave(8, 2, 64, 64, 16, [0, 0], [1, 1], seed=1)

@@ -1,4 +1,5 @@
-"""Plain, slow fp64 CPU oracle for paged chunked-prefill attention and the KV append.
+"""Plain, slow fp64 CPU oracles: paged chunked-prefill attention, the KV append, and chunked
+prefill of a KDA (gated delta-rule) layer with state snapshot and resume.
 
 TEST INFRASTRUCTURE ONLY.  Only the tests, the smoke check and the bench's CPU-baseline leg
 may import this package.  It shares no code with the HIP path: no kernels, helpers, tables or
@@ -19,3 +20,4 @@ from .attention import (  # noqa: F401
     probabilities,
     merge_partials,
 )
+from . import kda  # noqa: F401,E402

@@ -1,6 +1,8 @@
-"""Chunked-prefill attention over a paged KV cache on AMD MI355X (gfx950).
+"""Chunked-prefill attention over a paged KV cache, and chunked prefill of a KDA (gated
+delta-rule) layer with recurrent-state snapshots, on AMD MI355X (gfx950).
 
-Thin Python binding of libwavepp_attn.so (C ABI declared in include/wavepp_attn.h).  Every step of
+Thin Python binding of libwavepp_attn.so (C ABI declared in include/wavepp_attn.h and
+include/wavepp_kda.h).  Every step of
 the computation runs in the library's HIP kernels; this module only marshals arguments: torch
 tensors are passed as device pointers, the stream is torch's current HIP stream.
 
@@ -10,6 +12,12 @@ Per wave:
     plan_upload(p, ws)                  # enqueue the metadata copy
     append_kv(p, k_new, v_new, k_pool, v_pool, ws)
     chunked_prefill(p, q, k_pool, v_pool, out, lse, ws)
+
+Per wave of a KDA layer:
+    kp = kda_plan(...)                  # host: validate chunk lengths and snapshot slots
+    ws = new_workspace(kp)
+    kda_upload(kp, ws)
+    kda_chunked_prefill(kp, q, k, v, alpha, beta, state_pool, out, ws)
 """
 import ctypes
 import os
@@ -27,6 +35,10 @@ EXPORTED_SYMBOLS = [
     "wavepp_attn_plan", "wavepp_plan_workspace_bytes", "wavepp_plan_get_info", "wavepp_plan_get_items",
     "wavepp_attn_plan_upload", "wavepp_attn_append_kv", "wavepp_attn_chunked_prefill", "wavepp_plan_destroy",
     "wavepp_status_string", "wavepp_last_error",
+]
+KDA_SYMBOLS = [
+    "wavepp_kda_plan", "wavepp_kda_workspace_bytes", "wavepp_kda_get_info", "wavepp_kda_upload",
+    "wavepp_kda_chunked_prefill", "wavepp_kda_destroy",
 ]
 
 
@@ -55,6 +67,21 @@ class _Info(ctypes.Structure):
                 ("max_splits", ctypes.c_int32), ("rows_per_item", ctypes.c_int32), ("kv_tile", ctypes.c_int32),
                 ("partial_rows", ctypes.c_int64), ("metadata_bytes", ctypes.c_int64),
                 ("workspace_bytes", ctypes.c_int64)]
+
+
+class _KdaShape(ctypes.Structure):
+    _fields_ = [("num_heads", ctypes.c_int32), ("head_dim_k", ctypes.c_int32), ("head_dim_v", ctypes.c_int32),
+                ("num_state_slots", ctypes.c_int32)]
+
+
+class _KdaBatch(ctypes.Structure):
+    _fields_ = [("num_requests", ctypes.c_int32), ("chunk_lens", ctypes.POINTER(ctypes.c_int32)),
+                ("state_in", ctypes.POINTER(ctypes.c_int32)), ("state_out", ctypes.POINTER(ctypes.c_int32))]
+
+
+class _KdaInfo(ctypes.Structure):
+    _fields_ = [("total_tokens", ctypes.c_int64), ("num_items", ctypes.c_int32), ("block_tokens", ctypes.c_int32),
+                ("metadata_bytes", ctypes.c_int64), ("workspace_bytes", ctypes.c_int64)]
 
 
 _lib = None
@@ -90,6 +117,18 @@ def load_library(path: str = None) -> ctypes.CDLL:
     lib.wavepp_status_string.restype = ctypes.c_char_p
     lib.wavepp_last_error.argtypes = []
     lib.wavepp_last_error.restype = ctypes.c_char_p
+    lib.wavepp_kda_plan.argtypes = [ctypes.POINTER(_KdaShape), ctypes.POINTER(_KdaBatch), ctypes.POINTER(vp)]
+    lib.wavepp_kda_plan.restype = ctypes.c_int
+    lib.wavepp_kda_workspace_bytes.argtypes = [vp]
+    lib.wavepp_kda_workspace_bytes.restype = sz
+    lib.wavepp_kda_get_info.argtypes = [vp, ctypes.POINTER(_KdaInfo)]
+    lib.wavepp_kda_get_info.restype = ctypes.c_int
+    lib.wavepp_kda_upload.argtypes = [vp, vp, sz, vp]
+    lib.wavepp_kda_upload.restype = ctypes.c_int
+    lib.wavepp_kda_chunked_prefill.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.wavepp_kda_chunked_prefill.restype = ctypes.c_int
+    lib.wavepp_kda_destroy.argtypes = [vp]
+    lib.wavepp_kda_destroy.restype = None
     _lib = lib
     return lib
 
@@ -221,3 +260,79 @@ def chunked_prefill(p: Plan, q, k_pool, v_pool, out, lse, workspace, stream=None
         p.handle, _ptr(q, bf, "q"), _ptr(k_pool, bf, "k_pool"), _ptr(v_pool, bf, "v_pool"), _ptr(out, bf, "out"),
         _ptr(lse, torch.float32, "lse"), _ptr(workspace, name="workspace"),
         workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+# ------------------------------------------------------------------------------------------------
+# KDA chunked prefill
+# ------------------------------------------------------------------------------------------------
+
+class KdaPlan:
+    """A validated KDA wave: chunk lengths and snapshot slots (host object owned by the library)."""
+
+    def __init__(self, handle, shape):
+        self._h = ctypes.c_void_p(handle)
+        self.shape = shape
+
+    @property
+    def handle(self):
+        if not self._h:
+            raise ValueError("plan was destroyed")
+        return self._h
+
+    @property
+    def workspace_bytes(self) -> int:
+        return int(load_library().wavepp_kda_workspace_bytes(self.handle))
+
+    def info(self) -> dict:
+        info = _KdaInfo()
+        _check(load_library().wavepp_kda_get_info(self.handle, ctypes.byref(info)))
+        return {name: int(getattr(info, name)) for name, _ in _KdaInfo._fields_}
+
+    def destroy(self):
+        if self._h:
+            load_library().wavepp_kda_destroy(self._h)
+            self._h = ctypes.c_void_p(None)
+
+    def __del__(self):
+        try:
+            self.destroy()
+        except Exception:
+            pass
+
+
+def kda_plan(*, num_heads, head_dim_k, head_dim_v, num_state_slots, chunk_lens, state_in, state_out) -> KdaPlan:
+    lib = load_library()
+    chunk = np.ascontiguousarray(chunk_lens, dtype=np.int32)
+    s_in = np.ascontiguousarray(state_in, dtype=np.int32)
+    s_out = np.ascontiguousarray(state_out, dtype=np.int32)
+    if not (chunk.ndim == 1 and chunk.shape == s_in.shape == s_out.shape):
+        raise ValueError("chunk_lens, state_in and state_out must be 1-D of the same length")
+    shape = _KdaShape(num_heads, head_dim_k, head_dim_v, num_state_slots)
+    p32 = ctypes.POINTER(ctypes.c_int32)
+    batch = _KdaBatch(int(chunk.shape[0]), chunk.ctypes.data_as(p32), s_in.ctypes.data_as(p32),
+                      s_out.ctypes.data_as(p32))
+    out = ctypes.c_void_p()
+    _check(lib.wavepp_kda_plan(ctypes.byref(shape), ctypes.byref(batch), ctypes.byref(out)))
+    return KdaPlan(out.value, dict(num_heads=num_heads, head_dim_k=head_dim_k, head_dim_v=head_dim_v,
+                                   num_state_slots=num_state_slots, total_tokens=int(chunk.sum())))
+
+
+def kda_plan_for(spec) -> KdaPlan:
+    """Plan a wave described by a workloads.kda.KdaSpec-like object."""
+    return kda_plan(num_heads=spec.num_heads, head_dim_k=spec.head_dim_k, head_dim_v=spec.head_dim_v,
+                    num_state_slots=spec.num_slots, chunk_lens=spec.chunk_lens, state_in=spec.state_in,
+                    state_out=spec.state_out)
+
+
+def kda_upload(p: KdaPlan, workspace, stream=None):
+    _check(load_library().wavepp_kda_upload(p.handle, _ptr(workspace, name="workspace"),
+                                            workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def kda_chunked_prefill(p: KdaPlan, q, k, v, alpha, beta, state_pool, out, workspace, stream=None):
+    import torch
+    bf, f32 = torch.bfloat16, torch.float32
+    _check(load_library().wavepp_kda_chunked_prefill(
+        p.handle, _ptr(q, bf, "q"), _ptr(k, bf, "k"), _ptr(v, bf, "v"), _ptr(alpha, f32, "alpha"),
+        _ptr(beta, f32, "beta"), _ptr(state_pool, f32, "state_pool"), _ptr(out, bf, "out"),
+        _ptr(workspace, name="workspace"), workspace.numel() * workspace.element_size(), _stream(stream)))

@@ -45,12 +45,13 @@ struct wavepp_plan {
   size_t workspace_bytes = 0;
 };
 
+namespace wavepp {
 namespace {
-
 thread_local std::string g_last_error;
 std::atomic<uint32_t> g_serial{1};
+}  // namespace
 
-int fail(int status, const char* fmt, ...) {
+int set_error(int status, const char* fmt, ...) {
   char buf[512];
   va_list ap;
   va_start(ap, fmt);
@@ -60,9 +61,19 @@ int fail(int status, const char* fmt, ...) {
   return status;
 }
 
-int hip_fail(hipError_t e, const char* what) {
-  return fail(WAVEPP_EHIP, "%s: %s", what, hipGetErrorString(e));
+int set_hip_error(hipError_t e, const char* what) {
+  return set_error(WAVEPP_EHIP, "%s: %s", what, hipGetErrorString(e));
 }
+
+void clear_error() { g_last_error.clear(); }
+
+const char* last_error_text() { return g_last_error.c_str(); }
+
+uint32_t next_serial() { return g_serial.fetch_add(1); }
+
+}  // namespace wavepp
+
+namespace {
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
@@ -148,6 +159,10 @@ std::vector<WorkItem> order_items(std::vector<WorkItem> items, int G, bool xcd_a
   return out;
 }
 
+}  // namespace
+
+namespace wavepp {
+
 // ---------------------------------------------------------------------------------------------
 // Pinned staging for metadata uploads: a small ring of page-locked buffers per device, each
 // guarded by an event so a buffer is refilled only after its previous copy has completed.
@@ -169,7 +184,7 @@ constexpr int kStageSlots = 8;
 int stage_and_copy(const void* src, size_t bytes, void* dst, hipStream_t stream) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
-  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (e != hipSuccess) return set_hip_error(e, "hipGetDevice");
   std::lock_guard<std::mutex> lock(g_stage_mu);
   if (g_stage.size() <= size_t(dev)) g_stage.resize(dev + 1);
   DeviceStaging& ds = g_stage[dev];
@@ -178,11 +193,11 @@ int stage_and_copy(const void* src, size_t bytes, void* dst, hipStream_t stream)
   ds.next = (ds.next + 1) % ds.slots.size();
   if (!s.done) {
     e = hipEventCreateWithFlags(&s.done, hipEventDisableTiming);
-    if (e != hipSuccess) return hip_fail(e, "hipEventCreateWithFlags");
+    if (e != hipSuccess) return set_hip_error(e, "hipEventCreateWithFlags");
   }
   if (s.pending) {
     e = hipEventSynchronize(s.done);
-    if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+    if (e != hipSuccess) return set_hip_error(e, "hipEventSynchronize");
     s.pending = false;
   }
   if (s.cap < bytes) {
@@ -190,27 +205,31 @@ int stage_and_copy(const void* src, size_t bytes, void* dst, hipStream_t stream)
       e = hipHostFree(s.host);
       s.host = nullptr;
       s.cap = 0;
-      if (e != hipSuccess) return hip_fail(e, "hipHostFree");
+      if (e != hipSuccess) return set_hip_error(e, "hipHostFree");
     }
     size_t cap = align_up(std::max<size_t>(bytes, 64 << 10), 4096);
     e = hipHostMalloc(&s.host, cap, hipHostMallocDefault);
-    if (e != hipSuccess) return hip_fail(e, "hipHostMalloc");
+    if (e != hipSuccess) return set_hip_error(e, "hipHostMalloc");
     s.cap = cap;
   }
   memcpy(s.host, src, bytes);
   e = hipMemcpyAsync(dst, s.host, bytes, hipMemcpyHostToDevice, stream);
-  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync");
+  if (e != hipSuccess) return set_hip_error(e, "hipMemcpyAsync");
   e = hipEventRecord(s.done, stream);
-  if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
+  if (e != hipSuccess) return set_hip_error(e, "hipEventRecord");
   s.pending = true;
   return WAVEPP_OK;
 }
 
+}  // namespace wavepp
+
+namespace {
+
 int check_workspace(const wavepp_plan* plan, void* ws, size_t ws_bytes) {
-  if (!ws) return fail(WAVEPP_EINVAL, "workspace is NULL");
-  if (reinterpret_cast<uintptr_t>(ws) % 256) return fail(WAVEPP_EINVAL, "workspace must be 256-byte aligned");
+  if (!ws) return set_error(WAVEPP_EINVAL, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(ws) % 256) return set_error(WAVEPP_EINVAL, "workspace must be 256-byte aligned");
   if (ws_bytes < plan->workspace_bytes)
-    return fail(WAVEPP_ENOSPACE, "workspace has %zu bytes, plan needs %zu", ws_bytes, plan->workspace_bytes);
+    return set_error(WAVEPP_ENOSPACE, "workspace has %zu bytes, plan needs %zu", ws_bytes, plan->workspace_bytes);
   return WAVEPP_OK;
 }
 
@@ -260,32 +279,32 @@ const char* wavepp_status_string(int status) {
   }
 }
 
-const char* wavepp_last_error(void) { return g_last_error.c_str(); }
+const char* wavepp_last_error(void) { return last_error_text(); }
 
 int wavepp_attn_plan(const wavepp_attn_shape* shape, const wavepp_batch* batch, int32_t max_splits,
                      wavepp_plan** out) {
-  g_last_error.clear();
-  if (!shape || !batch || !out) return fail(WAVEPP_EINVAL, "null argument");
+  clear_error();
+  if (!shape || !batch || !out) return set_error(WAVEPP_EINVAL, "null argument");
   *out = nullptr;
   const wavepp_attn_shape s = *shape;
   if (s.num_q_heads <= 0 || s.num_kv_heads <= 0 || s.num_pages <= 0 || s.page_size <= 0 ||
       s.head_dim_qk <= 0 || s.head_dim_v <= 0)
-    return fail(WAVEPP_EINVAL, "non-positive shape field");
+    return set_error(WAVEPP_EINVAL, "non-positive shape field");
   if (!(s.softmax_scale > 0.0f) || !std::isfinite(s.softmax_scale))
-    return fail(WAVEPP_EINVAL, "softmax_scale must be positive and finite");
+    return set_error(WAVEPP_EINVAL, "softmax_scale must be positive and finite");
   if (s.num_q_heads % s.num_kv_heads)
-    return fail(WAVEPP_EINVAL, "num_q_heads (%d) is not a multiple of num_kv_heads (%d)", s.num_q_heads,
+    return set_error(WAVEPP_EINVAL, "num_q_heads (%d) is not a multiple of num_kv_heads (%d)", s.num_q_heads,
                 s.num_kv_heads);
-  if (s.kv_shared != 0 && s.kv_shared != 1) return fail(WAVEPP_EINVAL, "kv_shared must be 0 or 1");
+  if (s.kv_shared != 0 && s.kv_shared != 1) return set_error(WAVEPP_EINVAL, "kv_shared must be 0 or 1");
   if (!supported_shape(s))
-    return fail(WAVEPP_EUNSUPPORTED, "unsupported (head_dim_qk=%d, head_dim_v=%d, page_size=%d, kv_shared=%d, "
+    return set_error(WAVEPP_EUNSUPPORTED, "unsupported (head_dim_qk=%d, head_dim_v=%d, page_size=%d, kv_shared=%d, "
                 "num_kv_heads=%d)", s.head_dim_qk, s.head_dim_v, s.page_size, s.kv_shared, s.num_kv_heads);
-  if (max_splits < 0) return fail(WAVEPP_EINVAL, "max_splits must be >= 0");
+  if (max_splits < 0) return set_error(WAVEPP_EINVAL, "max_splits must be >= 0");
   const int32_t R = batch->num_requests;
-  if (R < 0) return fail(WAVEPP_EINVAL, "num_requests < 0");
+  if (R < 0) return set_error(WAVEPP_EINVAL, "num_requests < 0");
   if (R > 0 && (!batch->prefix_lens || !batch->chunk_lens || !batch->block_table))
-    return fail(WAVEPP_EINVAL, "null span or block-table array");
-  if (R > 0 && batch->bt_stride <= 0) return fail(WAVEPP_EINVAL, "bt_stride must be positive");
+    return set_error(WAVEPP_EINVAL, "null span or block-table array");
+  if (R > 0 && batch->bt_stride <= 0) return set_error(WAVEPP_EINVAL, "bt_stride must be positive");
   const int32_t B = s.page_size, P = s.num_pages, stride = R > 0 ? batch->bt_stride : 0;
   const int G = s.num_q_heads / s.num_kv_heads;
 
@@ -294,22 +313,22 @@ int wavepp_attn_plan(const wavepp_attn_shape* shape, const wavepp_batch* batch, 
   std::vector<int32_t> refcount(P, 0);
   for (int32_t r = 0; r < R; ++r) {
     const int64_t p = batch->prefix_lens[r], c = batch->chunk_lens[r];
-    if (p < 0 || c < 0) return fail(WAVEPP_EINVAL, "request %d: negative length (p=%lld, c=%lld)", r, (long long)p,
+    if (p < 0 || c < 0) return set_error(WAVEPP_EINVAL, "request %d: negative length (p=%lld, c=%lld)", r, (long long)p,
                                     (long long)c);
     const int64_t n = p + c;
-    if (n > INT32_MAX / 2) return fail(WAVEPP_EINVAL, "request %d: length %lld too large", r, (long long)n);
+    if (n > INT32_MAX / 2) return set_error(WAVEPP_EINVAL, "request %d: length %lld too large", r, (long long)n);
     if (n > int64_t(stride) * B)
-      return fail(WAVEPP_EPOSITION, "request %d: positions up to %lld but the block table covers %lld", r,
+      return set_error(WAVEPP_EPOSITION, "request %d: positions up to %lld but the block table covers %lld", r,
                   (long long)n, (long long)stride * B);
     const int64_t nb = ceil_div(n, B);
     const int32_t* row = batch->block_table + int64_t(r) * stride;
     for (int64_t b = 0; b < nb; ++b) {
       if (row[b] < 0 || row[b] >= P)
-        return fail(WAVEPP_ERANGE, "request %d block %lld: page %d outside [0, %d)", r, (long long)b, row[b], P);
+        return set_error(WAVEPP_ERANGE, "request %d block %lld: page %d outside [0, %d)", r, (long long)b, row[b], P);
       refcount[row[b]]++;
     }
     total += c;
-    if (total > INT32_MAX / 2) return fail(WAVEPP_EINVAL, "too many tokens in the wave");
+    if (total > INT32_MAX / 2) return set_error(WAVEPP_EINVAL, "too many tokens in the wave");
   }
   for (int32_t r = 0; r < R; ++r) {
     const int64_t p = batch->prefix_lens[r], c = batch->chunk_lens[r];
@@ -317,17 +336,17 @@ int wavepp_attn_plan(const wavepp_attn_shape* shape, const wavepp_batch* batch, 
     const int32_t* row = batch->block_table + int64_t(r) * stride;
     for (int64_t b = p / B; b < ceil_div(p + c, B); ++b)
       if (refcount[row[b]] != 1)
-        return fail(WAVEPP_EALIAS, "request %d block %lld: page %d receives appended tokens but is referenced %d "
+        return set_error(WAVEPP_EALIAS, "request %d block %lld: page %d receives appended tokens but is referenced %d "
                     "times in the wave", r, (long long)b, row[b], refcount[row[b]]);
   }
 
   auto plan = new (std::nothrow) wavepp_plan();
-  if (!plan) return fail(WAVEPP_EINVAL, "out of host memory");
+  if (!plan) return set_error(WAVEPP_EINVAL, "out of host memory");
   plan->shape = s;
   plan->num_requests = R;
   plan->bt_stride = stride;
   plan->total_tokens = total;
-  plan->serial = g_serial.fetch_add(1);
+  plan->serial = next_serial();
   const bool mla = s.kv_shared != 0;
   // grouped kernel: 8 waves (256 rows) per workgroup and one workgroup per CU, so that each K/V tile
   // staged in LDS serves 256 rows.  When no (request, KV head) has more than 128 rows (short
@@ -409,7 +428,7 @@ int wavepp_attn_plan(const wavepp_attn_shape* shape, const wavepp_batch* batch, 
     part_rows += S * w.rows;
     if (part_rows > INT32_MAX / 2) {
       delete plan;
-      return fail(WAVEPP_EINVAL, "split partials too large");
+      return set_error(WAVEPP_EINVAL, "split partials too large");
     }
   }
   plan->num_real_items = int32_t(items.size());
@@ -418,7 +437,7 @@ int wavepp_attn_plan(const wavepp_attn_shape* shape, const wavepp_batch* batch, 
   plan->items = order_items(std::move(items), G, env_flag("WAVEPP_XCD_ORDER", true));
   if (plan->items.size() > size_t(INT32_MAX / 2)) {
     delete plan;
-    return fail(WAVEPP_EINVAL, "too many work items");
+    return set_error(WAVEPP_EINVAL, "too many work items");
   }
 
   // --- metadata blob -------------------------------------------------------------------------------
@@ -459,7 +478,7 @@ int wavepp_attn_plan(const wavepp_attn_shape* shape, const wavepp_batch* batch, 
 size_t wavepp_plan_workspace_bytes(const wavepp_plan* plan) { return plan ? plan->workspace_bytes : 0; }
 
 int wavepp_plan_get_info(const wavepp_plan* plan, wavepp_plan_info* info) {
-  if (!plan || !info) return fail(WAVEPP_EINVAL, "null argument");
+  if (!plan || !info) return set_error(WAVEPP_EINVAL, "null argument");
   info->total_tokens = plan->total_tokens;
   info->num_items = int32_t(plan->items.size());
   info->num_real_items = plan->num_real_items;
@@ -474,7 +493,7 @@ int wavepp_plan_get_info(const wavepp_plan* plan, wavepp_plan_info* info) {
 }
 
 int wavepp_plan_get_items(const wavepp_plan* plan, int32_t* items, int32_t capacity) {
-  if (!plan || (!items && capacity > 0) || capacity < 0) return fail(WAVEPP_EINVAL, "bad argument");
+  if (!plan || (!items && capacity > 0) || capacity < 0) return set_error(WAVEPP_EINVAL, "bad argument");
   const int32_t n = std::min<int32_t>(capacity, int32_t(plan->items.size()));
   for (int32_t i = 0; i < n; ++i) {
     const WorkItem& w = plan->items[i];
@@ -485,8 +504,8 @@ int wavepp_plan_get_items(const wavepp_plan* plan, int32_t* items, int32_t capac
 }
 
 int wavepp_attn_plan_upload(const wavepp_plan* plan, void* workspace, size_t ws_bytes, hipStream_t stream) {
-  g_last_error.clear();
-  if (!plan) return fail(WAVEPP_EINVAL, "plan is NULL");
+  clear_error();
+  if (!plan) return set_error(WAVEPP_EINVAL, "plan is NULL");
   int st = check_workspace(plan, workspace, ws_bytes);
   if (st) return st;
   return stage_and_copy(plan->blob.data(), plan->blob.size(), workspace, stream);
@@ -494,43 +513,43 @@ int wavepp_attn_plan_upload(const wavepp_plan* plan, void* workspace, size_t ws_
 
 int wavepp_attn_append_kv(const wavepp_plan* plan, const void* k_new, const void* v_new, void* k_pool, void* v_pool,
                           void* workspace, size_t ws_bytes, hipStream_t stream) {
-  g_last_error.clear();
-  if (!plan) return fail(WAVEPP_EINVAL, "plan is NULL");
+  clear_error();
+  if (!plan) return set_error(WAVEPP_EINVAL, "plan is NULL");
   int st = check_workspace(plan, workspace, ws_bytes);
   if (st) return st;
   const bool shared = plan->shape.kv_shared != 0;
   if (plan->total_tokens == 0) return WAVEPP_OK;
-  if (!k_new || !k_pool) return fail(WAVEPP_EINVAL, "k_new / k_pool is NULL");
-  if (!shared && (!v_new || !v_pool)) return fail(WAVEPP_EINVAL, "v_new / v_pool is NULL");
-  if (shared && (v_new || v_pool)) return fail(WAVEPP_EINVAL, "v_new / v_pool must be NULL for a latent cache");
+  if (!k_new || !k_pool) return set_error(WAVEPP_EINVAL, "k_new / k_pool is NULL");
+  if (!shared && (!v_new || !v_pool)) return set_error(WAVEPP_EINVAL, "v_new / v_pool is NULL");
+  if (shared && (v_new || v_pool)) return set_error(WAVEPP_EINVAL, "v_new / v_pool must be NULL for a latent cache");
   if (!aligned16(k_new) || !aligned16(k_pool) || (!shared && (!aligned16(v_new) || !aligned16(v_pool))))
-    return fail(WAVEPP_EINVAL, "device buffers must be 16-byte aligned");
+    return set_error(WAVEPP_EINVAL, "device buffers must be 16-byte aligned");
   DevPlan d = make_dev(plan, workspace);
   hipError_t e = launch_append(d, k_new, v_new, k_pool, v_pool, stream);
-  if (e != hipSuccess) return hip_fail(e, "append_kv launch");
+  if (e != hipSuccess) return set_hip_error(e, "append_kv launch");
   return WAVEPP_OK;
 }
 
 int wavepp_attn_chunked_prefill(const wavepp_plan* plan, const void* q, const void* k_pool, const void* v_pool,
                                 void* out, float* lse, void* workspace, size_t ws_bytes, hipStream_t stream) {
-  g_last_error.clear();
-  if (!plan) return fail(WAVEPP_EINVAL, "plan is NULL");
+  clear_error();
+  if (!plan) return set_error(WAVEPP_EINVAL, "plan is NULL");
   int st = check_workspace(plan, workspace, ws_bytes);
   if (st) return st;
   const bool shared = plan->shape.kv_shared != 0;
   if (plan->total_tokens == 0) return WAVEPP_OK;
-  if (!q || !k_pool || !out) return fail(WAVEPP_EINVAL, "q / k_pool / out is NULL");
-  if (!shared && !v_pool) return fail(WAVEPP_EINVAL, "v_pool is NULL");
-  if (shared && v_pool) return fail(WAVEPP_EINVAL, "v_pool must be NULL for a latent cache");
+  if (!q || !k_pool || !out) return set_error(WAVEPP_EINVAL, "q / k_pool / out is NULL");
+  if (!shared && !v_pool) return set_error(WAVEPP_EINVAL, "v_pool is NULL");
+  if (shared && v_pool) return set_error(WAVEPP_EINVAL, "v_pool must be NULL for a latent cache");
   if (!aligned16(q) || !aligned16(k_pool) || !aligned16(out) || (!shared && !aligned16(v_pool)) ||
       (reinterpret_cast<uintptr_t>(lse) & 3))
-    return fail(WAVEPP_EINVAL, "device buffers must be 16-byte aligned (lse 4-byte)");
+    return set_error(WAVEPP_EINVAL, "device buffers must be 16-byte aligned (lse 4-byte)");
   DevPlan d = make_dev(plan, workspace);
   hipError_t e = launch_attention(d, q, k_pool, v_pool, out, lse, stream);
-  if (e != hipSuccess) return hip_fail(e, "attention launch");
+  if (e != hipSuccess) return set_hip_error(e, "attention launch");
   if (!plan->merges.empty()) {
     e = launch_merge(d, out, lse, stream);
-    if (e != hipSuccess) return hip_fail(e, "merge launch");
+    if (e != hipSuccess) return set_hip_error(e, "merge launch");
   }
   return WAVEPP_OK;
 }

@@ -75,6 +75,50 @@ struct DevPlan {
   float softmax_scale;
 };
 
+// ---------------------------------------------------------------------------------------------
+// KDA chunked prefill
+// ---------------------------------------------------------------------------------------------
+constexpr uint32_t kKdaMagic = 0x4B444131u;  // "KDA1"
+constexpr int kKdaBlock = 64;                // tokens per block of the chunkwise form
+constexpr int kKdaDim = 128;                 // d_k = d_v supported by the kernel
+
+struct alignas(16) KdaHeader {
+  uint32_t magic;
+  uint32_t serial;
+  int32_t num_items;
+  int32_t num_heads;
+};
+
+// One request of the wave with at least one token; a workgroup runs one (item, head).
+struct alignas(16) KdaItem {
+  int32_t req;
+  int32_t cu;         // first packed token
+  int32_t len;        // c_r > 0
+  int32_t state_in;   // snapshot slot to resume from, -1 = zero state
+  int32_t state_out;  // snapshot slot written with the final state
+  int32_t pad[3];
+};
+
+struct KdaDevPlan {
+  const KdaHeader* hdr;
+  const KdaItem* items;
+  uint32_t serial;
+  int32_t num_items;
+  int32_t num_heads;
+  int32_t num_slots;
+};
+
+hipError_t launch_kda_prefill(const KdaDevPlan& p, const void* q, const void* k, const void* v, const float* alpha,
+                              const float* beta, float* state_pool, void* out, hipStream_t stream);
+
+// Shared host helpers (host.cpp): thread-local error detail, pinned metadata staging, plan serials.
+int set_error(int status, const char* fmt, ...);
+int set_hip_error(hipError_t e, const char* what);
+void clear_error();
+const char* last_error_text();
+int stage_and_copy(const void* src, size_t bytes, void* dst, hipStream_t stream);
+uint32_t next_serial();
+
 hipError_t launch_append(const DevPlan& p, const void* k_new, const void* v_new, void* k_pool, void* v_pool,
                          hipStream_t stream);
 hipError_t launch_attention(const DevPlan& p, const void* q, const void* k_pool, const void* v_pool, void* out,

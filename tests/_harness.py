@@ -37,3 +37,31 @@ def gpu_wave(spec, t, max_splits=0, device="cuda", with_lse=True, plan=None):
 
 def out_f64(t):
     return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+# ------------------------------------------------------------------------------------------------
+# KDA chunked prefill
+# ------------------------------------------------------------------------------------------------
+
+def oracle_kda(spec, t, heads=None):
+    """Oracle KDA wave on CPU copies of the inputs: (o [T, len(heads), d_v], pool_after [slots, H, d_k, d_v])."""
+    bits = {n: wl.to_bits(t[n]) for n in ("q", "k", "v")}
+    return oracle.kda.chunked_prefill(bits["q"], bits["k"], bits["v"], t["alpha"].cpu().numpy(),
+                                      t["beta"].cpu().numpy(), t["state_pool"].cpu().numpy(), spec.chunk_lens,
+                                      spec.state_in, spec.state_out, heads=heads)
+
+
+def gpu_kda(spec, t, device="cuda", plan=None, pool=None):
+    """HIP path: plan, upload, chunked prefill.  Returns device tensors (out, state_pool)."""
+    import torch
+    import paper_2609_35263_amd as wp
+    d = {n: t[n].to(device).contiguous() for n in ("q", "k", "v", "alpha", "beta")}
+    pool = t["state_pool"].to(device).contiguous().clone() if pool is None else pool
+    p = plan or wp.kda_plan_for(spec)
+    ws = wp.new_workspace(p, device)
+    out = torch.full((spec.total_tokens, spec.num_heads, spec.head_dim_v), float("nan"), dtype=torch.bfloat16,
+                     device=device)
+    wp.kda_upload(p, ws)
+    wp.kda_chunked_prefill(p, d["q"], d["k"], d["v"], d["alpha"], d["beta"], pool, out, ws)
+    torch.cuda.synchronize()
+    return {"out": out, "state_pool": pool, "plan": p, "ws": ws, "dev": d}

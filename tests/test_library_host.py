@@ -13,10 +13,13 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 def test_library_loads_and_exports_every_declared_symbol():
     lib = wp.load_library()
-    header = open(os.path.join(ROOT, "include", "wavepp_attn.h")).read()
-    declared = set(re.findall(r"^(?:const\s+)?\w+\s*\*?\s*(wavepp_\w+)\s*\(", header, re.M))
+    declared = set()
+    for name in sorted(os.listdir(os.path.join(ROOT, "include"))):
+        if name.endswith(".h"):
+            header = open(os.path.join(ROOT, "include", name)).read()
+            declared |= set(re.findall(r"^(?:const\s+)?\w+\s*\*?\s*(wavepp_\w+)\s*\(", header, re.M))
     assert declared, "no declarations found"
-    assert declared == set(wp.EXPORTED_SYMBOLS)
+    assert declared == set(wp.EXPORTED_SYMBOLS) | set(wp.KDA_SYMBOLS)
     for name in declared:
         assert hasattr(lib, name), name
 

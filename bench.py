@@ -8,12 +8,21 @@ timed region.  Prints ONE JSON line.
 
 Metric: attention TFLOP/s (algorithmic FLOP = 2 * Hq * (d_qk + d_v) * sum_r [c_r p_r + c_r (c_r + 1) / 2]
 per layer, exact causal pairs only), new tokens/s, % of the bf16 dense MFMA peak.
+
+    python bench.py --config kda_wave|kda_long|kda_short|kda_small
+
+times the KDA chunked prefill instead (one layer per step: plan -> upload -> chunked prefill, resuming
+from and writing snapshots).  It is bound by HBM: its metric is new tokens/s and its roofline the
+algorithmic bytes per launch (q, k, v, alpha, beta, out, and the snapshots read and written) over the
+kernel time, against 8 TB/s.
 """
 import argparse
 import json
 import os
 import sys
 import time
+
+import numpy as np
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
@@ -120,6 +129,8 @@ def main():
         sys.exit(2)
     if args.measure_traffic:
         sys.exit(measure_traffic(args.config, args.measure_traffic))
+    if str(args.config).startswith("kda"):
+        return main_kda(args)
 
     import numpy as np
     import torch
@@ -255,6 +266,145 @@ def main():
     print(json.dumps(res), flush=True)
 
 
+KDA_METRIC = "KDA chunked-prefill new tokens/s on 1 GPU; % of HBM peak"
+
+
+def kda_bytes_alg(spec) -> float:
+    """Algorithmic HBM bytes of one KDA layer: q, k, v (bf16), alpha (fp32), beta (fp32) read once, out
+    (bf16) written once, and one fp32 snapshot per head read for each resumed request and written for
+    each active one."""
+    th = float(spec.total_tokens) * spec.num_heads
+    per_th = 2 * spec.head_dim_k * 2 + spec.head_dim_v * 2 + spec.head_dim_k * 4 + 4 + spec.head_dim_v * 2
+    active = spec.chunk_lens > 0
+    snaps = int(np.sum(active & (spec.state_in >= 0))) + int(np.sum(active))
+    return th * per_th + float(snaps) * spec.num_heads * spec.head_dim_k * spec.head_dim_v * 4
+
+
+def kda_flops_alg(spec) -> float:
+    """FLOP of the token-by-token recurrence per token and head: decay (d_k d_v), k^T S (2 d_k d_v), the
+    rank-1 erase-and-write (2 d_k d_v) and the read-out (2 d_k d_v)."""
+    return 7.0 * spec.head_dim_k * spec.head_dim_v * float(spec.total_tokens) * spec.num_heads
+
+
+def kda_cpu_baseline(spec, tensors, budget_s=12.0):
+    """Time the fp64 oracle (as it stands) on the host cores: the first n tokens of the first request,
+    all heads, n grown until the run takes a few seconds.  Reported in new tokens/s of the whole layer."""
+    import oracle.kda as okda
+    import workloads as wl
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    c0 = int(spec.chunk_lens[0])
+    n = 8
+    while True:
+        n = min(n, c0)
+        part = {k: tensors[k][:n].cpu() for k in ("q", "k", "v", "alpha", "beta")}
+        bits = {k: wl.to_bits(part[k]) for k in ("q", "k", "v")}
+        pool = tensors["state_pool"].cpu().numpy()
+        t0 = time.perf_counter()
+        okda.chunked_prefill(bits["q"], bits["k"], bits["v"], part["alpha"].numpy(), part["beta"].numpy(), pool,
+                             [n], [int(spec.state_in[0])], [int(spec.state_out[0])])
+        dt = time.perf_counter() - t0
+        if dt >= budget_s / 4 or n >= c0:
+            break
+        n = int(n * min(16.0, max(2.0, budget_s / 2 / max(dt, 1e-3))))
+    return {"value": round(n / dt, 3), "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"first {n} tokens of request 0 of the {spec.name} wave, all {spec.num_heads} heads",
+            "seconds": round(dt, 3)}
+
+
+def main_kda(args):
+    import torch
+    import paper_2609_35263_amd as wp
+    import workloads.kda as wk
+
+    wp.load_library()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    spec = wk.config(args.config)
+    t = wk.make_tensors(spec, seed=8000, device=dev, poison=False)
+    T = spec.total_tokens
+    out = torch.empty((T, spec.num_heads, spec.head_dim_v), dtype=torch.bfloat16, device=dev)
+    pool = t["state_pool"]
+    p0 = wp.kda_plan_for(spec)
+    ws = wp.new_workspace(p0, dev)
+    stream = torch.cuda.current_stream()
+    kev = []
+
+    def step(record=False):
+        p = wp.kda_plan_for(spec)
+        wp.kda_upload(p, ws)
+        if record:
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+        wp.kda_chunked_prefill(p, t["q"], t["k"], t["v"], t["alpha"], t["beta"], pool, out, ws)
+        if record:
+            e1.record(stream)
+            kev.append((e0, e1))
+
+    if args.copy_calibration_mib:
+        n = args.copy_calibration_mib << 20
+        src = torch.ones(n, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step(record=True)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms_per_step = elapsed * 1e3 / args.steps
+    kms = float(np.mean([a.elapsed_time(b) for a, b in kev]))
+    b = kda_bytes_alg(spec)
+    f = kda_flops_alg(spec)
+    gbps = b / (kms * 1e-3) / 1e9
+    traffic = None
+    tfile = os.path.join(ROOT, "profiles", f"traffic_{spec.name}.json")
+    if os.path.exists(tfile):
+        try:
+            tj = json.load(open(tfile))
+            if tj.get("kernel_source_hash") == _kernel_hash("kda"):
+                traffic = tj.get("bytes_per_launch")
+        except Exception:
+            traffic = None
+    res = {
+        "metric": KDA_METRIC,
+        "value": round(T / (ms_per_step * 1e-3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{spec.name}: {spec.num_requests} chunks of {int(spec.chunk_lens.min())}-"
+                               f"{int(spec.chunk_lens.max())} tokens ({T} new tokens), "
+                               f"{int(np.sum(spec.state_in >= 0))} resumed from snapshots, {spec.num_heads} heads, "
+                               f"d_k {spec.head_dim_k}, d_v {spec.head_dim_v}",
+                   "global_batch": int(spec.num_requests), "new_tokens": int(T), "layers": 1,
+                   "parallelism": "none (1 GPU)"},
+        "kda_kernel_ms": round(kms, 4),
+        "alg_TFLOPs_recurrence": round(f / (kms * 1e-3) / 1e12, 3),
+        "work_groups": int(p0.info()["num_items"]) * spec.num_heads,
+        "roofline": {"bound": "hbm", "achieved": round(gbps, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": round(gbps / PEAK_HBM_GBS, 4), "traffic": traffic, "kernel": "kda_prefill_kernel",
+                     "alg_bytes_per_launch": b, "alg_flop_per_launch": f},
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = kda_cpu_baseline(spec, wk.make_tensors(spec, seed=8000, device=dev, poison=False))
+    print(json.dumps(res), flush=True)
+
+
 def measure_traffic(config, out_json, calib_mib=1024):
     """Two rocprofv3 counter passes (FETCH_SIZE, then WRITE_SIZE) over a short run of this config.
 
@@ -265,7 +415,9 @@ def measure_traffic(config, out_json, calib_mib=1024):
     import csv
     import subprocess
     import tempfile
-    out = {"config": str(config), "kernel_source_hash": _kernel_hash(), "calibration_copy_mib": calib_mib}
+    kind = "kda" if str(config).startswith("kda") else "attn"
+    kname = "kda_prefill" if kind == "kda" else "attn_"
+    out = {"config": str(config), "kernel_source_hash": _kernel_hash(kind), "calibration_copy_mib": calib_mib}
     known_kib = calib_mib * 1024.0
     for counter in ("FETCH_SIZE", "WRITE_SIZE"):
         d = tempfile.mkdtemp(prefix=f"wavepp_{counter.lower()}_", dir=os.environ.get("TMPDIR", "/tmp"))
@@ -282,7 +434,7 @@ def measure_traffic(config, out_json, calib_mib=1024):
         if not rows:
             print(f"[traffic] no counter rows (rc={res.returncode})", file=sys.stderr)
             return 1
-        attn = [float(r["Counter_Value"]) for r in rows if "attn_" in r["Kernel_Name"]]
+        attn = [float(r["Counter_Value"]) for r in rows if kname in r["Kernel_Name"]]
         copy = [float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"]]
         if not attn or not copy:
             print("[traffic] attention or calibration copy kernel missing from the counter rows", file=sys.stderr)
@@ -299,10 +451,13 @@ def measure_traffic(config, out_json, calib_mib=1024):
     return 0
 
 
-def _kernel_hash():
+def _kernel_hash(kind="attn"):
+    """Hash of the sources that decide a kernel's memory traffic: its kernel file, its planner and the
+    shared layout header."""
     import hashlib
     h = hashlib.sha256()
-    for f in ("kernels.hip", "host.cpp", "internal.h"):
+    files = ("kernels.hip", "host.cpp", "internal.h") if kind == "attn" else ("kda.hip", "kda_host.cpp", "internal.h")
+    for f in files:
         h.update(open(os.path.join(ROOT, "paper_2609_35263_amd", "csrc", f), "rb").read())
     return h.hexdigest()[:16]
 

@@ -18,7 +18,9 @@
 // accumulation; the state itself stays in fp32 accumulators for the whole chunk.
 //
 // Range.  The factorization gamma_t / gamma_s = gamma_t * (1 / gamma_s) is used for a channel only
-// when its block decay gamma_C is at least 2^-96, so every factor stays a normal number.  A
+// when its block decay gamma_C is at least 2^-96, so every factor stays a normal number.  Kbar is
+// built from products of the later decays (gamma_C / gamma_s without a division) and
+// 1 / gamma_s = (gamma_C / gamma_s) / gamma_C, one reciprocal per channel and block.  A
 // channel that decays more within one block (including alpha = 0) is "slow": it contributes to A
 // and P through an exact pairwise term exp2(G_t - G_s) in log2 space instead, and its Kbar uses
 // exp2(G_C - G_s).
@@ -39,6 +41,8 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 constexpr int kC = kKdaBlock;       // tokens per block
 constexpr int kD = kKdaDim;         // d_k = d_v
@@ -57,18 +61,22 @@ struct KdaLds {
     float tf[kC * AS];              // T = (I + A)^-1 in fp32 while it is built
   };
   __bf16 kbt[kD * CS];              // Kbar^T                  [c][t]
-  __bf16 vt[kD * CS];               // V^T                     [j][t]
-  float a[kC * AS];                 // A (beta-scaled, strictly lower)
+  __bf16 v[kC * RS];                // V                       [t][j]
+  union {
+    float a[kC * AS];               // A (beta-scaled, strictly lower)
+    struct {                        // slow channels of one batch, log2-space
+      float g[kSlowBatch][kC];
+      float k[kSlowBatch][kC];
+      float q[kSlowBatch][kC];
+    } slow;
+  };
   __bf16 pm[kC * CS];               // P (lower incl. diagonal)
   __bf16 tm[kC * CS];               // T in bf16
-  float x[3][16 * 17];              // block products of the inversion
+  float x[2][16 * 17];              // 16-block products of the inversion
   float beta[kC];
   float gc[kD];                     // gamma_C per channel
-  float qtot[4][kD];                // per-quarter decay products
-  float ltot[4][kD];                // per-quarter log2-decay sums (slow channels)
-  float slow_g[kSlowBatch][kC];
-  float slow_k[kSlowBatch][kC];
-  float slow_q[kSlowBatch][kC];
+  float qtot[8][kD];                // per-octet decay products
+  int slow_list[kD];
 };
 
 __device__ __forceinline__ bool kda_meta_ok(const KdaDevPlan& p) {
@@ -88,6 +96,15 @@ __device__ __forceinline__ bf16x8 lds_a_perm(const __bf16* rowp, int base) {
   return cat(*reinterpret_cast<const bf16x4*>(rowp + base), *reinterpret_cast<const bf16x4*>(rowp + base + 8));
 }
 
+// The same from an fp32 row, rounded to bf16.
+__device__ __forceinline__ bf16x8 lds_a_perm_f32(const float* rowp, int base) {
+  const float4 lo = *reinterpret_cast<const float4*>(rowp + base);
+  const float4 hi = *reinterpret_cast<const float4*>(rowp + base + 8);
+  return bf16x8{static_cast<__bf16>(lo.x), static_cast<__bf16>(lo.y), static_cast<__bf16>(lo.z),
+                static_cast<__bf16>(lo.w), static_cast<__bf16>(hi.x), static_cast<__bf16>(hi.y),
+                static_cast<__bf16>(hi.z), static_cast<__bf16>(hi.w)};
+}
+
 // Registers 8kk .. 8kk+7 of an accumulator tile, rounded to bf16: a B operand in permuted order.
 __device__ __forceinline__ bf16x8 acc_to_b(const f32x16& acc, int kk) {
   bf16x8 r;
@@ -98,6 +115,50 @@ __device__ __forceinline__ bf16x8 acc_to_b(const f32x16& acc, int kk) {
 
 __device__ __forceinline__ f32x16 mfma(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// Transposing LDS read: within each group of 16 lanes, lane i receives element i%4 of the 8 bytes
+// addressed by lanes 4m + i/4, m = 0..3.
+__device__ __forceinline__ bf16x4 lds_read_tr(const __bf16* p) {
+  const i16x4 r = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p));
+  return __builtin_bit_cast(bf16x4, r);
+}
+
+// Workgroup barrier for LDS traffic only.  __syncthreads() also drains every outstanding global
+// load of the wave (its release fence covers all memory), which would stall on the next block's
+// prefetch; every exchange between waves here goes through LDS, so draining this wave's LDS
+// operations before the barrier is enough.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// Raw inputs of one block, as loaded by one thread: channels 4 cq .. 4 cq + 3 of tokens
+// 8 oc .. 8 oc + 7 (alpha, k, q), 32 values of one token (v) and one beta.
+struct RawBlock {
+  float4 a[8];
+  uint2 k[8], q[8];
+  uint4 v[4];
+  float b;
+};
+
+__device__ __forceinline__ void load_raw(RawBlock& r, const float* __restrict__ alpha, const __bf16* __restrict__ k,
+                                         const __bf16* __restrict__ q, const __bf16* __restrict__ v,
+                                         const float* __restrict__ beta, int64_t tok0, int L, int64_t tok_stride,
+                                         int64_t head_off, int head, int H, int tid) {
+  // Rows past the block's last token re-read its last row (always in bounds) and are replaced by
+  // neutral values (alpha = 1, k = q = v = 0, beta = 0) when they are consumed: no branches here.
+  const int cq = tid & 31, oc = tid >> 5;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int t = min(8 * oc + i, L - 1);
+    const int64_t base = (tok0 + t) * tok_stride + head_off + 4 * cq;
+    r.a[i] = *reinterpret_cast<const float4*>(alpha + base);
+    r.k[i] = *reinterpret_cast<const uint2*>(k + base);
+    r.q[i] = *reinterpret_cast<const uint2*>(q + base);
+  }
+  const int tv = min(tid >> 2, L - 1), part = tid & 3;
+  const uint4* src = reinterpret_cast<const uint4*>(v + (tok0 + tv) * tok_stride + head_off + 32 * part);
+#pragma unroll
+  for (int u = 0; u < 4; ++u) r.v[u] = src[u];
+  r.b = beta[(tok0 + min(tid, L - 1)) * H + head];
 }
 
 __global__ __launch_bounds__(256, 1) void kda_prefill_kernel(KdaDevPlan p, const __bf16* __restrict__ q,
@@ -117,156 +178,139 @@ __global__ __launch_bounds__(256, 1) void kda_prefill_kernel(KdaDevPlan p, const
   const int64_t tok_stride = int64_t(H) * kD;           // elements between tokens of one head
   const int64_t head_off = int64_t(head) * kD;
   const int j0 = 32 * wave;                             // this wave's state columns
+  const int cq = tid & 31, oc = tid >> 5;               // phase 0: channels 4 cq + e, tokens 8 oc + i
 
   // ---- state S0 (fp32) -------------------------------------------------------------------------
   // tile ib, register 4b + r: row i = 32 ib + 8 b + 4 hf + r, column j0 + col
   f32x16 S[4];
-  {
+#pragma unroll
+  for (int ib = 0; ib < 4; ++ib) S[ib] = f32x16{};
+  if (it.state_in >= 0) {
     const float* src = state_pool + (int64_t(it.state_in) * H + head) * kD * kD + j0 + col;
 #pragma unroll
     for (int ib = 0; ib < 4; ++ib)
 #pragma unroll
-      for (int reg = 0; reg < 16; ++reg) {
-        const int i = 32 * ib + 8 * (reg >> 2) + 4 * hf + (reg & 3);
-        S[ib][reg] = it.state_in >= 0 ? src[int64_t(i) * kD] : 0.0f;
-      }
+      for (int reg = 0; reg < 16; ++reg)
+        S[ib][reg] = src[int64_t(32 * ib + 8 * (reg >> 2) + 4 * hf + (reg & 3)) * kD];
   }
 
-  const int ch0 = 2 * lane;        // phase-0 channels of this thread: ch0, ch0 + 1
-  const int qq = wave;             // phase-0 token quarter: [16 qq, 16 qq + 16)
+  RawBlock raw;
+  load_raw(raw, alpha, k, q, v, beta, it.cu, min(kC, it.len), tok_stride, head_off, head, H, tid);
 
   for (int blk = 0; blk < it.len; blk += kC) {
     const int L = min(kC, it.len - blk);
     const int64_t tok0 = int64_t(it.cu) + blk;
 
-    // ================= phase 0: decays, scaled operands, V^T, beta ==============================
-    float g0[16], g1[16];          // running decay product within the quarter
-    uint32_t kraw[16], qraw[16];   // bf16 pairs (ch0, ch0 + 1)
-    float run0 = 1.0f, run1 = 1.0f;
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int t = 16 * qq + i;
-      float2 a2 = make_float2(1.0f, 1.0f);
-      uint32_t kr2 = 0, qr2 = 0;
-      if (t < L) {
-        const int64_t base = (tok0 + t) * tok_stride + head_off + ch0;
-        a2 = *reinterpret_cast<const float2*>(alpha + base);
-        kr2 = *reinterpret_cast<const uint32_t*>(k + base);
-        qr2 = *reinterpret_cast<const uint32_t*>(q + base);
-      }
-      run0 *= a2.x;
-      run1 *= a2.y;
-      g0[i] = run0;
-      g1[i] = run1;
-      kraw[i] = kr2;
-      qraw[i] = qr2;
-    }
-    ls.qtot[qq][ch0] = run0;
-    ls.qtot[qq][ch0 + 1] = run1;
-    if (tid < kC) ls.beta[tid] = tid < L ? beta[(tok0 + tid) * H + head] : 0.0f;
+    // ================= phase 0: decays, scaled operands, V, beta ================================
+    float g[8][4];                 // running decay product within the octet, inclusive
+    float sfx[8][4];               // decay product of the later tokens of the octet, exclusive
     {
-      // V^T: thread -> (token, 32-column part)
-      const int t = tid >> 2, part = tid & 3;
-      uint4 raw[4] = {};
-      if (t < L) {
-        const uint4* src = reinterpret_cast<const uint4*>(v + (tok0 + t) * tok_stride + head_off + 32 * part);
 #pragma unroll
-        for (int u = 0; u < 4; ++u) raw[u] = src[u];
-      }
-      const __bf16* e = reinterpret_cast<const __bf16*>(raw);
-#pragma unroll
-      for (int jj = 0; jj < 32; ++jj) ls.vt[(32 * part + jj) * CS + t] = e[jj];
-    }
-    __syncthreads();
-
-    float pre0 = 1.0f, pre1 = 1.0f, tot0 = 1.0f, tot1 = 1.0f;
-#pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      const float x0 = ls.qtot[w][ch0], x1 = ls.qtot[w][ch0 + 1];
-      if (w < qq) {
-        pre0 *= x0;
-        pre1 *= x1;
-      }
-      tot0 *= x0;
-      tot1 *= x1;
-    }
-    const bool slow0 = !(tot0 >= kFastFloor), slow1 = !(tot1 >= kFastFloor);
-    const int any_slow = __syncthreads_or(int(slow0 || slow1));
-
-    // log2-space decays of slow channels
-    float lg0[16], lg1[16], G0pre = 0.0f, G1pre = 0.0f, G0C = 0.0f, G1C = 0.0f;
-    int nslow = 0, idx0 = 0, idx1 = 0;
-    if (any_slow) {
-      float s0 = 0.0f, s1 = 0.0f;
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int t = 16 * qq + i;
-        float l0 = 0.0f, l1 = 0.0f;
-        if (t < L && (slow0 || slow1)) {
-          const float2 a2 = *reinterpret_cast<const float2*>(alpha + (tok0 + t) * tok_stride + head_off + ch0);
-          l0 = fmaxf(__log2f(a2.x), kLogFloor);
-          l1 = fmaxf(__log2f(a2.y), kLogFloor);
-          if (!(a2.x > 0.0f)) l0 = kLogFloor;
-          if (!(a2.y > 0.0f)) l1 = kLogFloor;
+      for (int i = 0; i < 8; ++i)
+        if (8 * oc + i >= L) {     // rows past the end: neutral
+          raw.a[i] = make_float4(1.0f, 1.0f, 1.0f, 1.0f);
+          raw.k[i] = make_uint2(0, 0);
+          raw.q[i] = make_uint2(0, 0);
         }
-        s0 += l0;
-        s1 += l1;
-        lg0[i] = s0;
-        lg1[i] = s1;
-      }
-      ls.ltot[qq][ch0] = s0;
-      ls.ltot[qq][ch0 + 1] = s1;
-      __syncthreads();
+      float run[4] = {1.0f, 1.0f, 1.0f, 1.0f}, back[4] = {1.0f, 1.0f, 1.0f, 1.0f};
 #pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        const float x0 = ls.ltot[w][ch0], x1 = ls.ltot[w][ch0 + 1];
-        if (w < qq) {
-          G0pre += x0;
-          G1pre += x1;
+      for (int i = 0; i < 8; ++i) {
+        const float ai[4] = {raw.a[i].x, raw.a[i].y, raw.a[i].z, raw.a[i].w};
+        const float aj[4] = {raw.a[7 - i].x, raw.a[7 - i].y, raw.a[7 - i].z, raw.a[7 - i].w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          run[e] *= ai[e];
+          g[i][e] = run[e];
+          sfx[7 - i][e] = back[e];
+          back[e] *= aj[e];
         }
-        G0C += x0;
-        G1C += x1;
       }
-      // compact index of the slow channels, in channel order (every wave sees all channels)
-      const uint64_t b0 = __ballot(slow0), b1 = __ballot(slow1);
-      const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-      idx0 = __popcll(b0 & below) + __popcll(b1 & below);
-      idx1 = idx0 + (slow0 ? 1 : 0);
-      nslow = __popcll(b0) + __popcll(b1);
+      *reinterpret_cast<float4*>(&ls.qtot[oc][4 * cq]) = make_float4(run[0], run[1], run[2], run[3]);
+      const int tv = tid >> 2, part = tid & 3;
+      const bool vok = tv < L;
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        *reinterpret_cast<uint4*>(&ls.v[tv * RS + 32 * part + 8 * u]) = vok ? raw.v[u] : make_uint4(0, 0, 0, 0);
+      if (tid < kC) ls.beta[tid] = tid < L ? raw.b : 0.0f;
     }
+    lds_barrier();
 
-    // scaled operands
+    float tot[4], pre[4], post[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      tot[e] = 1.0f;
+      pre[e] = 1.0f;
+      post[e] = 1.0f;
+    }
+#pragma unroll
+    for (int o = 0; o < 8; ++o) {
+      const float4 x = *reinterpret_cast<const float4*>(&ls.qtot[o][4 * cq]);
+      const float xs[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        if (o < oc) pre[e] *= xs[e];
+        if (o > oc) post[e] *= xs[e];
+        tot[e] *= xs[e];
+      }
+    }
+    // gamma_t = pre * g, gamma_C / gamma_t = sfx * post (a product of the later decays, no division),
+    // and k / gamma_t = (k gamma_C / gamma_t) / gamma_C: one reciprocal per channel
+    bool slow[4];
+    float inv_tot[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      slow[e] = !(tot[e] >= kFastFloor);
+      inv_tot[e] = slow[e] ? 0.0f : __frcp_rn(tot[e]);
+    }
     {
-      __bf16 kb0[16], kb1[16];
+      __bf16 kb[4][8];
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int t = 16 * qq + i;
-        const float gm0 = pre0 * g0[i], gm1 = pre1 * g1[i];
-        const float k0 = bf_lo(kraw[i]), k1 = bf_hi(kraw[i]);
-        const float q0 = bf_lo(qraw[i]), q1 = bf_hi(qraw[i]);
-        *reinterpret_cast<bf16x2*>(&ls.qt[t * RS + ch0]) = bf16x2{static_cast<__bf16>(q0 * gm0), static_cast<__bf16>(q1 * gm1)};
-        *reinterpret_cast<bf16x2*>(&ls.kt[t * RS + ch0]) = bf16x2{static_cast<__bf16>(k0 * gm0), static_cast<__bf16>(k1 * gm1)};
-        const float r0 = slow0 ? 0.0f : k0 * __frcp_rn(gm0);
-        const float r1 = slow1 ? 0.0f : k1 * __frcp_rn(gm1);
-        *reinterpret_cast<bf16x2*>(&ls.kr[t * RS + ch0]) = bf16x2{static_cast<__bf16>(r0), static_cast<__bf16>(r1)};
-        const float kb0f = slow0 ? k0 * exp2f(G0C - (G0pre + lg0[i])) : r0 * tot0;
-        const float kb1f = slow1 ? k1 * exp2f(G1C - (G1pre + lg1[i])) : r1 * tot1;
-        kb0[i] = static_cast<__bf16>(kb0f);
-        kb1[i] = static_cast<__bf16>(kb1f);
+      for (int i = 0; i < 8; ++i) {
+        const int t = 8 * oc + i;
+        const float kf[4] = {bf_lo(raw.k[i].x), bf_hi(raw.k[i].x), bf_lo(raw.k[i].y), bf_hi(raw.k[i].y)};
+        const float qf[4] = {bf_lo(raw.q[i].x), bf_hi(raw.q[i].x), bf_lo(raw.q[i].y), bf_hi(raw.q[i].y)};
+        bf16x4 vq, vk, vr;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float gm = pre[e] * g[i][e];
+          vq[e] = static_cast<__bf16>(qf[e] * gm);
+          vk[e] = static_cast<__bf16>(kf[e] * gm);
+          const float kbar = slow[e] ? 0.0f : kf[e] * (sfx[i][e] * post[e]);
+          vr[e] = static_cast<__bf16>(kbar * inv_tot[e]);
+          kb[e][i] = static_cast<__bf16>(kbar);
+        }
+        *reinterpret_cast<bf16x4*>(&ls.qt[t * RS + 4 * cq]) = vq;
+        *reinterpret_cast<bf16x4*>(&ls.kt[t * RS + 4 * cq]) = vk;
+        *reinterpret_cast<bf16x4*>(&ls.kr[t * RS + 4 * cq]) = vr;
       }
 #pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        *reinterpret_cast<bf16x8*>(&ls.kbt[ch0 * CS + 16 * qq + 8 * u]) =
-            bf16x8{kb0[8 * u], kb0[8 * u + 1], kb0[8 * u + 2], kb0[8 * u + 3], kb0[8 * u + 4], kb0[8 * u + 5], kb0[8 * u + 6], kb0[8 * u + 7]};
-        *reinterpret_cast<bf16x8*>(&ls.kbt[(ch0 + 1) * CS + 16 * qq + 8 * u]) =
-            bf16x8{kb1[8 * u], kb1[8 * u + 1], kb1[8 * u + 2], kb1[8 * u + 3], kb1[8 * u + 4], kb1[8 * u + 5], kb1[8 * u + 6], kb1[8 * u + 7]};
+      for (int e = 0; e < 4; ++e)
+        *reinterpret_cast<bf16x8*>(&ls.kbt[(4 * cq + e) * CS + 8 * oc]) =
+            bf16x8{kb[e][0], kb[e][1], kb[e][2], kb[e][3], kb[e][4], kb[e][5], kb[e][6], kb[e][7]};
+      if (oc == 0) *reinterpret_cast<float4*>(&ls.gc[4 * cq]) = make_float4(tot[0], tot[1], tot[2], tot[3]);
+    }
+    // compact list of the slow channels, in channel order (lanes 0-31 of every wave see all channels)
+    int nslow = 0;
+    {
+      const uint64_t lo32 = (lane < 32) ? ((lane == 0) ? 0ull : (~0ull >> (64 - lane))) : 0ull;
+      int below = 0;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const uint64_t b = __ballot(slow[e] && lane < 32);
+        below += __popcll(b & lo32);
+        nslow += __popcll(b);
       }
-      if (qq == 0) {
-        ls.gc[ch0] = tot0;
-        ls.gc[ch0 + 1] = tot1;
+      if (wave == 0 && lane < 32) {
+        int idx = below;
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (slow[e]) ls.slow_list[idx++] = 4 * cq + e;
       }
     }
-    __syncthreads();
+    // prefetch the next block's inputs; they arrive while this block is computed
+    if (blk + kC < it.len)
+      load_raw(raw, alpha, k, q, v, beta, tok0 + kC, min(kC, it.len - blk - kC), tok_stride, head_off, head, H, tid);
+    lds_barrier();
 
     // ================= phase 1: A and P (waves 0-2: tiles (0,0), (1,0), (1,1)) ====================
     const int tb1 = wave == 0 ? 0 : 1, sb1 = wave == 2 ? 1 : 0;
@@ -281,53 +325,76 @@ __global__ __launch_bounds__(256, 1) void kda_prefill_kernel(KdaDevPlan p, const
         accP = mfma(aq, b, accP);
       }
     }
-    // exact pairwise terms of slow channels, in batches
+    // slow channels: exact pairwise terms in log2 space, 16 channels per batch, re-read from memory
     for (int base = 0; base < nslow; base += kSlowBatch) {
-      __syncthreads();
-      if (slow0 && idx0 >= base && idx0 < base + kSlowBatch) {
+      lds_barrier();
+      const int cl = tid >> 4, tg = tid & 15;
+      const bool have = base + cl < nslow;
+      const int ch = have ? ls.slow_list[base + cl] : 0;
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int t = 16 * qq + i;
-          ls.slow_g[idx0 - base][t] = G0pre + lg0[i];
-          ls.slow_k[idx0 - base][t] = bf_lo(kraw[i]);
-          ls.slow_q[idx0 - base][t] = bf_lo(qraw[i]);
+      for (int u = 0; u < 4; ++u) {
+        const int t = 4 * tg + u;
+        float lg = 0.0f, kv = 0.0f, qv = 0.0f;
+        if (have && t < L) {
+          const int64_t idx = (tok0 + t) * tok_stride + head_off + ch;
+          const float a1 = alpha[idx];
+          lg = a1 > 0.0f ? fmaxf(__log2f(a1), kLogFloor) : kLogFloor;
+          kv = static_cast<float>(k[idx]);
+          qv = static_cast<float>(q[idx]);
+        }
+        ls.slow.g[cl][t] = lg;
+        ls.slow.k[cl][t] = kv;
+        ls.slow.q[cl][t] = qv;
+      }
+      lds_barrier();
+      if (tid < kSlowBatch) {
+        float run = 0.0f;
+        for (int t = 0; t < kC; ++t) {
+          run += ls.slow.g[tid][t];
+          ls.slow.g[tid][t] = run;
         }
       }
-      if (slow1 && idx1 >= base && idx1 < base + kSlowBatch) {
+      lds_barrier();
+      if (have) {
+        const float gC = ls.slow.g[cl][kC - 1];
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int t = 16 * qq + i;
-          ls.slow_g[idx1 - base][t] = G1pre + lg1[i];
-          ls.slow_k[idx1 - base][t] = bf_hi(kraw[i]);
-          ls.slow_q[idx1 - base][t] = bf_hi(qraw[i]);
+        for (int u = 0; u < 4; ++u) {
+          const int t = 4 * tg + u;
+          ls.kbt[ch * CS + t] = static_cast<__bf16>(ls.slow.k[cl][t] * exp2f(gC - ls.slow.g[cl][t]));
         }
       }
-      __syncthreads();
       if (wave < 3) {
         const int nb = min(kSlowBatch, nslow - base);
         const int s = 32 * sb1 + col;
         for (int c = 0; c < nb; ++c) {
-          const float gs = ls.slow_g[c][s], ks = ls.slow_k[c][s];
+          const float gs = ls.slow.g[c][s], ks = ls.slow.k[c][s];
 #pragma unroll
           for (int reg = 0; reg < 16; ++reg) {
             const int t = 32 * tb1 + 8 * (reg >> 2) + 4 * hf + (reg & 3);
-            const float e = exp2f(fminf(ls.slow_g[c][t] - gs, 0.0f)) * ks;
-            accA[reg] += ls.slow_k[c][t] * e;
-            accP[reg] += ls.slow_q[c][t] * e;
+            const float e = exp2f(fminf(ls.slow.g[c][t] - gs, 0.0f)) * ks;
+            accA[reg] += ls.slow.k[c][t] * e;
+            accP[reg] += ls.slow.q[c][t] * e;
           }
         }
       }
     }
+    if (nslow > 0) lds_barrier();   // the batch scratch shares storage with A
     if (wave < 3) {
       const int s = 32 * sb1 + col;
 #pragma unroll
-      for (int reg = 0; reg < 16; ++reg) {
-        const int t = 32 * tb1 + 8 * (reg >> 2) + 4 * hf + (reg & 3);
-        ls.a[t * AS + s] = s < t ? accA[reg] * ls.beta[t] : 0.0f;
-        ls.pm[t * CS + s] = static_cast<__bf16>(s <= t ? accP[reg] : 0.0f);
+      for (int b = 0; b < 4; ++b) {
+        const int t0 = 32 * tb1 + 8 * b + 4 * hf;
+        const float4 bt = *reinterpret_cast<const float4*>(&ls.beta[t0]);
+        const float bs[4] = {bt.x, bt.y, bt.z, bt.w};
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int t = t0 + r;
+          ls.a[t * AS + s] = s < t ? accA[4 * b + r] * bs[r] : 0.0f;
+          ls.pm[t * CS + s] = static_cast<__bf16>(s <= t ? accP[4 * b + r] : 0.0f);
+        }
       }
     }
-    __syncthreads();
+    lds_barrier();
 
     // ================= phase 2: T = (I + A)^-1 ==================================================
     {
@@ -344,38 +411,76 @@ __global__ __launch_bounds__(256, 1) void kda_prefill_kernel(KdaDevPlan p, const
       if (lane < 16) {
 #pragma unroll
         for (int t = 0; t < 16; ++t) ls.tf[(a0 + t) * AS + a0 + jc] = xs[t];
+        // the block right of an even diagonal block lies above the diagonal of its 32 x 32 block
+        if ((wave & 1) == 0) {
+#pragma unroll
+          for (int t = 0; t < 16; ++t) ls.tf[(a0 + t) * AS + a0 + 16 + jc] = 0.0f;
+        }
       }
     }
-    __syncthreads();
+    lds_barrier();
     {
-      // off-diagonal blocks by distance d: T_ab = -D_a sum_{c=b}^{a-1} A_ac T_cb
-      const int tr = tid >> 4, jc = tid & 15;
-      for (int d = 1; d < 4; ++d) {
-        for (int bi = 0; bi < 4 - d; ++bi) {
-          const int ba = bi + d, bb = bi;
-          float acc = 0.0f;
-          for (int c = bb; c < ba; ++c)
+      // 16 -> 32: T_ab = -D_a A_ab D_b for (a, b) = (1, 0) and (3, 2); two elements per thread
+      const int which = tid >> 7, e = tid & 127, tr = e >> 3, jc = 2 * (e & 7);
+      const int ba = 2 * which + 1, bb = 2 * which;
+      float x0 = 0.0f, x1 = 0.0f;
 #pragma unroll
-            for (int u = 0; u < 16; ++u)
-              acc += ls.a[(16 * ba + tr) * AS + 16 * c + u] * ls.tf[(16 * c + u) * AS + 16 * bb + jc];
-          ls.x[bi][tr * 17 + jc] = acc;
-        }
-        __syncthreads();
-        for (int bi = 0; bi < 4 - d; ++bi) {
-          const int ba = bi + d, bb = bi;
-          float acc = 0.0f;
-#pragma unroll
-          for (int u = 0; u < 16; ++u) acc -= ls.tf[(16 * ba + tr) * AS + 16 * ba + u] * ls.x[bi][u * 17 + jc];
-          ls.tf[(16 * ba + tr) * AS + 16 * bb + jc] = acc;
-        }
-        __syncthreads();
+      for (int u = 0; u < 16; ++u) {
+        const float av = ls.a[(16 * ba + tr) * AS + 16 * bb + u];
+        const float2 d = *reinterpret_cast<const float2*>(&ls.tf[(16 * bb + u) * AS + 16 * bb + jc]);
+        x0 += av * d.x;
+        x1 += av * d.y;
       }
-      for (int e = tid; e < kC * kC; e += 256) {
-        const int t = e >> 6, s = e & 63;
-        ls.tm[t * CS + s] = static_cast<__bf16>((s >> 4) <= (t >> 4) ? ls.tf[t * AS + s] : 0.0f);
+      ls.x[which][tr * 17 + jc] = x0;
+      ls.x[which][tr * 17 + jc + 1] = x1;
+      lds_barrier();
+      float y0 = 0.0f, y1 = 0.0f;
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        const float dv = ls.tf[(16 * ba + tr) * AS + 16 * ba + u];
+        y0 -= dv * ls.x[which][u * 17 + jc];
+        y1 -= dv * ls.x[which][u * 17 + jc + 1];
+      }
+      ls.tf[(16 * ba + tr) * AS + 16 * bb + jc] = y0;
+      ls.tf[(16 * ba + tr) * AS + 16 * bb + jc + 1] = y1;
+    }
+    lds_barrier();
+    if (wave == 0) {
+      // 32 -> 64 on the matrix cores: T21 = -T2 (A21 T1)
+      f32x16 xacc = {};
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        const float* arow = &ls.a[(32 + col) * AS + 16 * kk + 8 * hf];
+        const float4 lo = *reinterpret_cast<const float4*>(arow), hi = *reinterpret_cast<const float4*>(arow + 4);
+        const bf16x8 aop{static_cast<__bf16>(lo.x), static_cast<__bf16>(lo.y), static_cast<__bf16>(lo.z),
+                         static_cast<__bf16>(lo.w), static_cast<__bf16>(hi.x), static_cast<__bf16>(hi.y),
+                         static_cast<__bf16>(hi.z), static_cast<__bf16>(hi.w)};
+        bf16x8 bop;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) bop[e] = static_cast<__bf16>(ls.tf[(16 * kk + 8 * hf + e) * AS + col]);
+        xacc = mfma(aop, bop, xacc);
+      }
+      f32x16 yacc = {};
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+        yacc = mfma(lds_a_perm_f32(&ls.tf[(32 + col) * AS + 32], 16 * kk + 4 * hf), acc_to_b(xacc, kk), yacc);
+#pragma unroll
+      for (int reg = 0; reg < 16; ++reg) {
+        const int m = 8 * (reg >> 2) + 4 * hf + (reg & 3);
+        ls.tm[(32 + m) * CS + col] = static_cast<__bf16>(-yacc[reg]);
+      }
+    } else {
+      // diagonal 32-blocks to bf16 (zero above the diagonal 16-blocks): 2 x 32 rows x 4 segments of 8
+      for (int sgi = tid - 64; sgi < 256; sgi += 192) {
+        const int blk32 = sgi >> 7, row = (sgi >> 2) & 31, seg = sgi & 3;
+        const int t = 32 * blk32 + row, s0 = 32 * blk32 + 8 * seg;
+        bf16x8 w;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) w[e] = static_cast<__bf16>(((s0 + e) >> 4) <= (t >> 4) ? ls.tf[t * AS + s0 + e] : 0.0f);
+        *reinterpret_cast<bf16x8*>(&ls.tm[t * CS + s0]) = w;
       }
     }
-    __syncthreads();
+    lds_barrier();
 
     // ================= phase 3: the state chain (wave -> 32 state columns) =======================
     {
@@ -387,29 +492,31 @@ __global__ __launch_bounds__(256, 1) void kda_prefill_kernel(KdaDevPlan p, const
       }
       f32x16 accE[2] = {}, accO[2] = {};
 #pragma unroll
-      for (int tb = 0; tb < 2; ++tb) {
-        const __bf16* ktr = &ls.kt[(32 * tb + col) * RS];
-        const __bf16* qtr = &ls.qt[(32 * tb + col) * RS];
+      for (int ib = 0; ib < 4; ++ib)
 #pragma unroll
-        for (int ib = 0; ib < 4; ++ib)
+        for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
-          for (int kk = 0; kk < 2; ++kk) {
+          for (int tb = 0; tb < 2; ++tb) {
             const int cb = 32 * ib + 16 * kk + 4 * hf;
-            accE[tb] = mfma(lds_a_perm(ktr, cb), sB[ib][kk], accE[tb]);
-            accO[tb] = mfma(lds_a_perm(qtr, cb), sB[ib][kk], accO[tb]);
+            accE[tb] = mfma(lds_a_perm(&ls.kt[(32 * tb + col) * RS], cb), sB[ib][kk], accE[tb]);
+            accO[tb] = mfma(lds_a_perm(&ls.qt[(32 * tb + col) * RS], cb), sB[ib][kk], accO[tb]);
           }
-      }
-      // R = beta (V - E), in place in accE
+      // R = beta (V - E), in place in accE.  V[t0 + r][j] for r = 0..3 comes from the transposing
+      // read: lane 4m + g of each 16-lane group addresses row t0 + m at column 4g of its group.
       const int j = j0 + col;
+      const int grp = lane >> 4, li = lane & 15;
+      const int jg = j0 + 16 * (grp & 1) + 4 * (li & 3);
 #pragma unroll
       for (int tb = 0; tb < 2; ++tb)
 #pragma unroll
         for (int b = 0; b < 4; ++b) {
           const int t0 = 32 * tb + 8 * b + 4 * hf;
-          const bf16x4 vv = *reinterpret_cast<const bf16x4*>(&ls.vt[j * CS + t0]);
+          const bf16x4 vv = lds_read_tr(&ls.v[(t0 + (li >> 2)) * RS + jg]);
+          const float4 bt = *reinterpret_cast<const float4*>(&ls.beta[t0]);
+          const float bs[4] = {bt.x, bt.y, bt.z, bt.w};
 #pragma unroll
           for (int r = 0; r < 4; ++r)
-            accE[tb][4 * b + r] = ls.beta[t0 + r] * (static_cast<float>(vv[r]) - accE[tb][4 * b + r]);
+            accE[tb][4 * b + r] = bs[r] * (static_cast<float>(vv[r]) - accE[tb][4 * b + r]);
         }
       bf16x8 rB[2][2];
 #pragma unroll
@@ -451,7 +558,13 @@ __global__ __launch_bounds__(256, 1) void kda_prefill_kernel(KdaDevPlan p, const
 #pragma unroll
       for (int ib = 0; ib < 4; ++ib) {
 #pragma unroll
-        for (int reg = 0; reg < 16; ++reg) S[ib][reg] *= ls.gc[32 * ib + 8 * (reg >> 2) + 4 * hf + (reg & 3)];
+        for (int b = 0; b < 4; ++b) {
+          const float4 gcv = *reinterpret_cast<const float4*>(&ls.gc[32 * ib + 8 * b + 4 * hf]);
+          S[ib][4 * b + 0] *= gcv.x;
+          S[ib][4 * b + 1] *= gcv.y;
+          S[ib][4 * b + 2] *= gcv.z;
+          S[ib][4 * b + 3] *= gcv.w;
+        }
         const __bf16* kr = &ls.kbt[(32 * ib + col) * CS];
 #pragma unroll
         for (int sb = 0; sb < 2; ++sb)
@@ -459,7 +572,7 @@ __global__ __launch_bounds__(256, 1) void kda_prefill_kernel(KdaDevPlan p, const
           for (int kk = 0; kk < 2; ++kk) S[ib] = mfma(lds_a_perm(kr, 32 * sb + 16 * kk + 4 * hf), uB[sb][kk], S[ib]);
       }
     }
-    __syncthreads();
+    lds_barrier();
   }
 
   // ---- snapshot at the chunk boundary ---------------------------------------------------------

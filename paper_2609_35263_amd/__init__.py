@@ -36,6 +36,10 @@ EXPORTED_SYMBOLS = [
     "wavepp_attn_plan_upload", "wavepp_attn_append_kv", "wavepp_attn_chunked_prefill", "wavepp_plan_destroy",
     "wavepp_status_string", "wavepp_last_error",
 ]
+MPU_SYMBOLS = [
+    "wavepp_mpu_budget_ladder", "wavepp_mpu_create", "wavepp_mpu_admit", "wavepp_mpu_plan", "wavepp_mpu_commit",
+    "wavepp_mpu_retire", "wavepp_mpu_get_state", "wavepp_mpu_destroy",
+]
 KDA_SYMBOLS = [
     "wavepp_kda_plan", "wavepp_kda_workspace_bytes", "wavepp_kda_get_info", "wavepp_kda_upload",
     "wavepp_kda_chunked_prefill", "wavepp_kda_destroy",
@@ -84,6 +88,20 @@ class _KdaInfo(ctypes.Structure):
                 ("metadata_bytes", ctypes.c_int64), ("workspace_bytes", ctypes.c_int64)]
 
 
+class _MpuConfig(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("max_budget", "min_budget", "block", "stages", "fills", "max_lanes",
+                                               "split_permille", "count_inflight")]
+
+
+class _Span(ctypes.Structure):
+    _fields_ = [("request", ctypes.c_int32), ("start", ctypes.c_int32), ("length", ctypes.c_int32)]
+
+
+class _MpuState(ctypes.Structure):
+    _fields_ = [("work", ctypes.c_int64), ("budget", ctypes.c_int32), ("ring", ctypes.c_int32),
+                ("requests", ctypes.c_int32), ("up_count", ctypes.c_int32), ("down_count", ctypes.c_int32)]
+
+
 _lib = None
 
 
@@ -129,6 +147,19 @@ def load_library(path: str = None) -> ctypes.CDLL:
     lib.wavepp_kda_chunked_prefill.restype = ctypes.c_int
     lib.wavepp_kda_destroy.argtypes = [vp]
     lib.wavepp_kda_destroy.restype = None
+    cfgp, spanp = ctypes.POINTER(_MpuConfig), ctypes.POINTER(_Span)
+    lib.wavepp_mpu_budget_ladder.argtypes = [cfgp, ctypes.POINTER(i32), i32]
+    lib.wavepp_mpu_create.argtypes = [cfgp, ctypes.POINTER(vp)]
+    lib.wavepp_mpu_admit.argtypes = [vp, i32, i32, i32]
+    lib.wavepp_mpu_plan.argtypes = [vp, i32, spanp, i32, ctypes.POINTER(i32)]
+    lib.wavepp_mpu_commit.argtypes = [vp, spanp, i32]
+    lib.wavepp_mpu_retire.argtypes = [vp]
+    lib.wavepp_mpu_get_state.argtypes = [vp, ctypes.POINTER(_MpuState)]
+    lib.wavepp_mpu_destroy.argtypes = [vp]
+    lib.wavepp_mpu_destroy.restype = None
+    for name in ("wavepp_mpu_budget_ladder", "wavepp_mpu_create", "wavepp_mpu_admit", "wavepp_mpu_plan",
+                 "wavepp_mpu_commit", "wavepp_mpu_retire", "wavepp_mpu_get_state"):
+        getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -336,3 +367,67 @@ def kda_chunked_prefill(p: KdaPlan, q, k, v, alpha, beta, state_pool, out, works
         p.handle, _ptr(q, bf, "q"), _ptr(k, bf, "k"), _ptr(v, bf, "v"), _ptr(alpha, f32, "alpha"),
         _ptr(beta, f32, "beta"), _ptr(state_pool, f32, "state_pool"), _ptr(out, bf, "out"),
         _ptr(workspace, name="workspace"), workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+# ------------------------------------------------------------------------------------------------
+# MPU wave planner (host only)
+# ------------------------------------------------------------------------------------------------
+
+def _mpu_config(max_budget, min_budget, block, stages, fills, max_lanes, split_permille=125, count_inflight=True):
+    return _MpuConfig(max_budget, min_budget, block, stages, fills, max_lanes, split_permille, int(bool(count_inflight)))
+
+
+def mpu_budget_ladder(max_budget, min_budget, block) -> list:
+    cfg = _mpu_config(max_budget, min_budget, block, 1, 1, 1)
+    buf = (ctypes.c_int32 * 64)()
+    n = load_library().wavepp_mpu_budget_ladder(ctypes.byref(cfg), buf, 64)
+    if n < 0:
+        _check(n)
+    return list(buf[:n])
+
+
+class MpuPlanner:
+    """The native wave planner: admit requests, then plan / commit waves and retire them."""
+
+    def __init__(self, *, max_budget, min_budget, block, stages, fills, max_lanes, split_permille=125,
+                 count_inflight=True):
+        self.config = _mpu_config(max_budget, min_budget, block, stages, fills, max_lanes, split_permille,
+                                  count_inflight)
+        h = ctypes.c_void_p()
+        _check(load_library().wavepp_mpu_create(ctypes.byref(self.config), ctypes.byref(h)))
+        self._h = h
+        self._spans = (_Span * max(1, max_lanes))()
+
+    def admit(self, request, start, end):
+        _check(load_library().wavepp_mpu_admit(self._h, int(request), int(start), int(end)))
+
+    def plan(self, admission_pending=False):
+        b = ctypes.c_int32()
+        n = load_library().wavepp_mpu_plan(self._h, int(bool(admission_pending)), self._spans, len(self._spans),
+                                            ctypes.byref(b))
+        if n < 0:
+            _check(n)
+        return [(s.request, s.start, s.length) for s in self._spans[:n]], int(b.value)
+
+    def commit(self, spans):
+        arr = (_Span * max(1, len(spans)))(*[_Span(int(r), int(s), int(l)) for r, s, l in spans])
+        serial = load_library().wavepp_mpu_commit(self._h, arr, len(spans))
+        if serial < 0:
+            _check(serial)
+        return serial
+
+    def retire(self):
+        _check(load_library().wavepp_mpu_retire(self._h))
+
+    def state(self) -> dict:
+        st = _MpuState()
+        _check(load_library().wavepp_mpu_get_state(self._h, ctypes.byref(st)))
+        return {name: int(getattr(st, name)) for name, _ in _MpuState._fields_}
+
+    def __del__(self):
+        try:
+            if self._h:
+                load_library().wavepp_mpu_destroy(self._h)
+                self._h = None
+        except Exception:
+            pass

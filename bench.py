@@ -15,6 +15,11 @@ times the KDA chunked prefill instead (one layer per step: plan -> upload -> chu
 from and writing snapshots).  It is bound by HBM: its metric is new tokens/s and its roofline the
 algorithmic bytes per launch (q, k, v, alpha, beta, out, and the snapshots read and written) over the
 kernel time, against 8 TB/s.
+
+    python bench.py --config mpu
+
+times the native MPU wave planner on the host (planning decisions per second over a seeded admission
+trace shaped like the paper's eight-stage runs), against the reference planner as the CPU baseline.
 """
 import argparse
 import json
@@ -131,6 +136,8 @@ def main():
         sys.exit(measure_traffic(args.config, args.measure_traffic))
     if str(args.config).startswith("kda"):
         return main_kda(args)
+    if str(args.config) == "mpu":
+        return main_mpu(args)
 
     import numpy as np
     import torch
@@ -402,6 +409,91 @@ def main_kda(args):
     }
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = kda_cpu_baseline(spec, wk.make_tensors(spec, seed=8000, device=dev, poison=False))
+    print(json.dumps(res), flush=True)
+
+
+MPU_CONFIG = dict(max_budget=16384, min_budget=8192, block=64, stages=8, fills=1, max_lanes=64,
+                  count_inflight=False)
+
+
+def mpu_trace(planner, n_requests=512, concurrency=64, seed=9000):
+    """Drive a planner through one admission trace: requests with 10 % uncached suffixes of 65,536,
+    131,072 or 262,144-token prompts (and a quarter cold), at most `concurrency` in the system; every
+    proposed wave is accepted and the oldest wave retires when the ring is full.  Returns
+    (decisions, waves, seconds spent inside plan + commit)."""
+    rng = np.random.default_rng(seed)
+    lengths = [65536, 131072, 262144]
+    live, admitted, decisions, waves, spent = {}, 0, 0, 0, 0.0
+    R = 2 * MPU_CONFIG["stages"]
+    ring = 0
+    while admitted < n_requests or live:
+        while admitted < n_requests and len(live) < concurrency:
+            L = int(rng.choice(lengths))
+            cached = 0 if rng.random() < 0.25 else (L * 9 // 10) // 64 * 64
+            planner.admit(admitted, cached, L)
+            live[admitted] = L
+            admitted += 1
+        t0 = time.perf_counter()
+        spans, _ = planner.plan(admission_pending=admitted < n_requests)
+        if spans:
+            planner.commit(spans)
+        spent += time.perf_counter() - t0
+        decisions += 1
+        if spans:
+            waves += 1
+            ring += 1
+            for rid, st, ln in spans:
+                if st + ln >= live[rid]:
+                    del live[rid]
+        if ring >= R or not spans:
+            if ring:
+                planner.retire()
+                ring -= 1
+    return decisions, waves, spent
+
+
+def main_mpu(args):
+    import paper_2609_35263_amd as wp
+    import oracle.mpu as omp
+    wp.load_library()
+    reps = max(1, args.steps)
+    for _ in range(args.warmup):
+        mpu_trace(wp.MpuPlanner(**MPU_CONFIG), n_requests=64)
+    t0 = time.perf_counter()
+    dec = spent = 0
+    for _ in range(reps):
+        d, w, s = mpu_trace(wp.MpuPlanner(**MPU_CONFIG))
+        dec += d
+        spent += s
+    elapsed = time.perf_counter() - t0
+    res = {
+        "metric": "MPU wave-planner decisions/s on the host (plan + commit)",
+        "value": round(dec / spent, 1),
+        "unit": "decisions/s",
+        "n_gpus": 1,
+        "steps": reps,
+        "warmup": args.warmup,
+        "ms_per_step": round(elapsed * 1e3 / reps, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int32",
+        "data": "synthetic",
+        "config": {"workload": "512 requests at concurrency 64: 10 % suffixes of 65,536 / 131,072 / 262,144-token "
+                               "prompts (a quarter cold); P = 8 stages, M = 16,384, b_min = 8,192, F = 1, "
+                               "unscheduled tokens only, up to 64 requests per wave",
+                   "global_batch": 512, "parallelism": "none (host)"},
+        "us_per_decision": round(spent / dec * 1e6, 3),
+        "decisions_per_trace": dec // reps,
+        "waves_per_trace": w,
+        "roofline": None,
+    }
+    if not args.no_cpu_baseline:
+        t1 = time.perf_counter()
+        d, w2, s = mpu_trace(omp.Planner(**MPU_CONFIG))
+        res["cpu_baseline"] = {"value": round(d / s, 1), "unit": "decisions/s", "cores": 1, "kind": "oracle",
+                               "sample": "one full trace through the reference planner", "seconds": round(time.perf_counter() - t1, 3),
+                               "same_waves": w2 == w}
     print(json.dumps(res), flush=True)
 
 

@@ -20,6 +20,12 @@ kernel time, against 8 TB/s.
 
 times the native MPU wave planner on the host (planning decisions per second over a seeded admission
 trace shaped like the paper's eight-stage runs), against the reference planner as the CPU baseline.
+
+    python bench.py --config hints
+
+times reuse-hint discovery on the host: chained block hashing of 200K-token requests and the
+gallop/bisect prefix probe against a sharded index holding 64 such cached prompts (the paper's
+stress shape), with the plain scan and the reference as comparisons.
 """
 import argparse
 import json
@@ -138,6 +144,8 @@ def main():
         return main_kda(args)
     if str(args.config) == "mpu":
         return main_mpu(args)
+    if str(args.config) == "hints":
+        return main_hints(args)
 
     import numpy as np
     import torch
@@ -494,6 +502,92 @@ def main_mpu(args):
         res["cpu_baseline"] = {"value": round(d / s, 1), "unit": "decisions/s", "cores": 1, "kind": "oracle",
                                "sample": "one full trace through the reference planner", "seconds": round(time.perf_counter() - t1, 3),
                                "same_waves": w2 == w}
+    print(json.dumps(res), flush=True)
+
+
+def main_hints(args, n_req=64, prompt=200_000, block=64, seed=9100):
+    import paper_2609_35263_amd as wp
+    import oracle.hints as ohi
+    wp.load_library()
+    rng = np.random.default_rng(seed)
+    # 64 cached prompts of 200K tokens: groups of 8 share a common prefix of 0-100 % of the prompt
+    bases = [rng.integers(0, 150_000, prompt) for _ in range(8)]
+    idx = wp.HintIndex(num_shards=64)
+    cached = []
+    for i in range(n_req):
+        b = bases[i % 8]
+        cut = int(rng.integers(0, prompt // block + 1)) * block
+        seq = np.concatenate([b[:cut], rng.integers(0, 150_000, prompt - cut)])
+        _, keys = wp.block_hashes(seq, block)
+        idx.add(0, keys)
+        cached.append(keys)
+    # requests: another 64 prompts over the same bases
+    reqs = []
+    t_hash = []
+    for i in range(n_req):
+        b = bases[i % 8]
+        cut = int(rng.integers(0, prompt // block + 1)) * block
+        seq = np.concatenate([b[:cut], rng.integers(0, 150_000, prompt - cut)]).astype(np.int32)
+        t0 = time.perf_counter()
+        _, keys = wp.block_hashes(seq, block)
+        t_hash.append(time.perf_counter() - t0)
+        reqs.append(keys)
+    reps = max(1, args.steps)
+    gal, lin, probes_g, probes_l = [], [], [], []
+    for _ in range(args.warmup):
+        for k in reqs:
+            idx.probe_prefix(0, k)
+    for _ in range(reps):
+        for k in reqs:
+            t0 = time.perf_counter()
+            e, pg = idx.probe_prefix(0, k)
+            gal.append(time.perf_counter() - t0)
+            t0 = time.perf_counter()
+            e2, pl = idx.probe_prefix_linear(0, k)
+            lin.append(time.perf_counter() - t0)
+            assert e == e2
+            probes_g.append(pg)
+            probes_l.append(pl)
+    med = float(np.median(gal)) * 1e6
+    res = {
+        "metric": "reuse-hint prefix probe latency on the host (median, gallop + bisect)",
+        "value": round(med, 3),
+        "unit": "us",
+        "n_gpus": 1,
+        "steps": reps,
+        "warmup": args.warmup,
+        "ms_per_step": round(float(np.sum(gal)) * 1e3 / reps, 3),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "uint64",
+        "data": "synthetic",
+        "config": {"workload": f"{n_req} cached prompts of {prompt} tokens (blocks of {block}, 8 shared-prefix "
+                               f"families) in a 64-shard index; {n_req} request prompts probed",
+                   "global_batch": n_req, "parallelism": "none (host)"},
+        "p99_us": round(float(np.percentile(gal, 99)) * 1e6, 3),
+        "median_probes": int(np.median(probes_g)),
+        "linear_scan_median_us": round(float(np.median(lin)) * 1e6, 3),
+        "linear_scan_median_probes": int(np.median(probes_l)),
+        "hash_ms_per_request": round(float(np.median(t_hash)) * 1e3, 3),
+        "hash_MBps": round(prompt * 4 / float(np.median(t_hash)) / 1e6, 1),
+        "index_entries": idx.size(),
+        "roofline": None,
+    }
+    if not args.no_cpu_baseline:
+        ref = ohi.HintIndex()
+        for keys in cached:
+            ref.add(0, [int(x) for x in keys])
+        t0 = time.perf_counter()
+        times = []
+        for k in reqs:
+            kl = [int(x) for x in k]
+            t1 = time.perf_counter()
+            ohi.prefix_endpoint(ref, 0, kl)
+            times.append(time.perf_counter() - t1)
+        res["cpu_baseline"] = {"value": round(float(np.median(times)) * 1e6, 3), "unit": "us", "cores": 1,
+                               "kind": "oracle", "sample": f"the {n_req} request prompts, plain scan in the reference",
+                               "seconds": round(time.perf_counter() - t0, 3)}
     print(json.dumps(res), flush=True)
 
 

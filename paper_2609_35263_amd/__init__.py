@@ -40,6 +40,11 @@ MPU_SYMBOLS = [
     "wavepp_mpu_budget_ladder", "wavepp_mpu_create", "wavepp_mpu_admit", "wavepp_mpu_plan", "wavepp_mpu_commit",
     "wavepp_mpu_retire", "wavepp_mpu_get_state", "wavepp_mpu_destroy",
 ]
+HINT_SYMBOLS = [
+    "wavepp_block_hashes", "wavepp_hint_index_create", "wavepp_hint_index_add", "wavepp_hint_index_detach",
+    "wavepp_hint_index_size", "wavepp_hint_probe_prefix", "wavepp_hint_probe_prefix_linear",
+    "wavepp_hint_probe_recurrent", "wavepp_hint_index_destroy",
+]
 KDA_SYMBOLS = [
     "wavepp_kda_plan", "wavepp_kda_workspace_bytes", "wavepp_kda_get_info", "wavepp_kda_upload",
     "wavepp_kda_chunked_prefill", "wavepp_kda_destroy",
@@ -157,6 +162,21 @@ def load_library(path: str = None) -> ctypes.CDLL:
     lib.wavepp_mpu_get_state.argtypes = [vp, ctypes.POINTER(_MpuState)]
     lib.wavepp_mpu_destroy.argtypes = [vp]
     lib.wavepp_mpu_destroy.restype = None
+    i64, u64p, u8p = ctypes.c_int64, ctypes.POINTER(ctypes.c_uint64), ctypes.POINTER(ctypes.c_uint8)
+    lib.wavepp_block_hashes.argtypes = [ctypes.POINTER(i32), i64, i32, ctypes.POINTER(i64), i32, u8p, i32, u8p, u64p]
+    lib.wavepp_block_hashes.restype = i64
+    lib.wavepp_hint_index_create.argtypes = [i32, ctypes.POINTER(vp)]
+    lib.wavepp_hint_index_add.argtypes = [vp, i32, u64p, i64]
+    lib.wavepp_hint_index_detach.argtypes = [vp, i32, u64p, i64]
+    lib.wavepp_hint_index_size.argtypes = [vp]
+    lib.wavepp_hint_index_size.restype = i64
+    for name in ("wavepp_hint_probe_prefix", "wavepp_hint_probe_prefix_linear", "wavepp_hint_probe_recurrent"):
+        getattr(lib, name).argtypes = [vp, i32, u64p, i64, ctypes.POINTER(i64), ctypes.POINTER(i32)]
+        getattr(lib, name).restype = ctypes.c_int
+    for name in ("wavepp_hint_index_create", "wavepp_hint_index_add", "wavepp_hint_index_detach"):
+        getattr(lib, name).restype = ctypes.c_int
+    lib.wavepp_hint_index_destroy.argtypes = [vp]
+    lib.wavepp_hint_index_destroy.restype = None
     for name in ("wavepp_mpu_budget_ladder", "wavepp_mpu_create", "wavepp_mpu_admit", "wavepp_mpu_plan",
                  "wavepp_mpu_commit", "wavepp_mpu_retire", "wavepp_mpu_get_state"):
         getattr(lib, name).restype = ctypes.c_int
@@ -428,6 +448,80 @@ class MpuPlanner:
         try:
             if self._h:
                 load_library().wavepp_mpu_destroy(self._h)
+                self._h = None
+        except Exception:
+            pass
+
+
+# ------------------------------------------------------------------------------------------------
+# Reuse hints (host only)
+# ------------------------------------------------------------------------------------------------
+
+def block_hashes(tokens, block, extra_keys=None, salt=b""):
+    """Chained block hashes of the full blocks: (digests uint8 [n, 32], keys uint64 [n])."""
+    toks = np.ascontiguousarray(tokens, dtype=np.int32)
+    nb = len(toks) // int(block)
+    extra = None if extra_keys is None else np.ascontiguousarray(extra_keys, dtype=np.int64).reshape(nb, -1)
+    per = 0 if extra is None else int(extra.shape[1])
+    dig = np.zeros((max(nb, 1), 32), dtype=np.uint8)
+    keys = np.zeros(max(nb, 1), dtype=np.uint64)
+    salt_arr = np.frombuffer(bytes(salt), dtype=np.uint8) if salt else np.zeros(1, dtype=np.uint8)
+    n = load_library().wavepp_block_hashes(
+        toks.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), len(toks), int(block),
+        None if extra is None else extra.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), per,
+        salt_arr.ctypes.data_as(ctypes.POINTER(ctypes.c_uint8)), len(salt),
+        dig.ctypes.data_as(ctypes.POINTER(ctypes.c_uint8)), keys.ctypes.data_as(ctypes.POINTER(ctypes.c_uint64)))
+    if n < 0:
+        _check(int(n))
+    return dig[:n], keys[:n]
+
+
+class HintIndex:
+    """The native sharded counted index of (window, key)."""
+
+    def __init__(self, num_shards=64):
+        h = ctypes.c_void_p()
+        _check(load_library().wavepp_hint_index_create(int(num_shards), ctypes.byref(h)))
+        self._h = h
+
+    @staticmethod
+    def _keys(keys):
+        k = np.ascontiguousarray(keys, dtype=np.uint64)
+        return k, k.ctypes.data_as(ctypes.POINTER(ctypes.c_uint64))
+
+    def add(self, window, keys):
+        k, p = self._keys(keys)
+        _check(load_library().wavepp_hint_index_add(self._h, int(window), p, len(k)))
+
+    def detach(self, window, keys):
+        k, p = self._keys(keys)
+        _check(load_library().wavepp_hint_index_detach(self._h, int(window), p, len(k)))
+
+    def size(self):
+        return int(load_library().wavepp_hint_index_size(self._h))
+
+    def _probe(self, fn, window, keys, n):
+        k, p = self._keys(keys)
+        e, np_ = ctypes.c_int64(), ctypes.c_int32()
+        _check(getattr(load_library(), fn)(self._h, int(window), p, int(n), ctypes.byref(e), ctypes.byref(np_)))
+        return int(e.value), int(np_.value)
+
+    def probe_prefix(self, window, keys):
+        """(endpoint in blocks, probes) by gallop and bisect."""
+        return self._probe("wavepp_hint_probe_prefix", window, keys, len(keys))
+
+    def probe_prefix_linear(self, window, keys):
+        return self._probe("wavepp_hint_probe_prefix_linear", window, keys, len(keys))
+
+    def probe_recurrent(self, window, keys, limit):
+        if not 0 <= limit <= len(keys):
+            raise ValueError("limit outside [0, len(keys)]")
+        return self._probe("wavepp_hint_probe_recurrent", window, keys, limit)
+
+    def __del__(self):
+        try:
+            if self._h:
+                load_library().wavepp_hint_index_destroy(self._h)
                 self._h = None
         except Exception:
             pass

@@ -625,9 +625,10 @@ def measure_traffic(config, out_json, calib_mib=1024):
         if not attn or not copy:
             print("[traffic] attention or calibration copy kernel missing from the counter rows", file=sys.stderr)
             return 1
-        factor = known_kib / copy[0]
+        calib = max(copy)          # the 1 GiB calibration copy; other device copies are far smaller
+        factor = known_kib / calib
         out[counter] = {"kib_per_launch": sum(attn) / len(attn), "launches": len(attn),
-                        "calibration_kib": copy[0], "factor": factor,
+                        "calibration_kib": calib, "factor": factor,
                         "bytes_per_launch": sum(attn) / len(attn) * factor * 1024.0}
     out["bytes_per_launch"] = out["FETCH_SIZE"]["bytes_per_launch"] + out["WRITE_SIZE"]["bytes_per_launch"]
     out["command"] = f"python bench.py --config {config} --measure-traffic {out_json}"

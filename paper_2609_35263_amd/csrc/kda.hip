@@ -59,6 +59,7 @@ struct KdaLds {
   union {
     __bf16 kr[kC * RS];             // K_R = k / gamma (0 for slow channels)   [t][c]
     float tf[kC * AS];              // T = (I + A)^-1 in fp32 while it is built
+    __bf16 ob[kC * RS];             // the block's output rows, staged for 16-byte stores
   };
   __bf16 kbt[kD * CS];              // Kbar^T                  [c][t]
   __bf16 v[kC * RS];                // V                       [t][j]
@@ -551,7 +552,7 @@ __global__ __launch_bounds__(256, 1) void kda_prefill_kernel(KdaDevPlan p, const
 #pragma unroll
         for (int reg = 0; reg < 16; ++reg) {
           const int t = 32 * tb + 8 * (reg >> 2) + 4 * hf + (reg & 3);
-          if (t < L) out[(tok0 + t) * tok_stride + head_off + j] = static_cast<__bf16>(accO[tb][reg]);
+          ls.ob[t * RS + j] = static_cast<__bf16>(accO[tb][reg]);
         }
       }
       // S = Diag(gamma_C) S + Kbar^T U
@@ -573,6 +574,16 @@ __global__ __launch_bounds__(256, 1) void kda_prefill_kernel(KdaDevPlan p, const
       }
     }
     lds_barrier();
+    // the block's output rows leave from LDS as 16-byte stores (the next block writes this storage
+    // only after its first barrier)
+    {
+      const int t = tid >> 2, part = tid & 3;
+      if (t < L) {
+        uint4* dst = reinterpret_cast<uint4*>(out + (tok0 + t) * tok_stride + head_off + 32 * part);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) dst[u] = *reinterpret_cast<const uint4*>(&ls.ob[t * RS + 32 * part + 8 * u]);
+      }
+    }
   }
 
   // ---- snapshot at the chunk boundary ---------------------------------------------------------

@@ -140,26 +140,44 @@ struct RawBlock {
   float b;
 };
 
-__device__ __forceinline__ void load_raw(RawBlock& r, const float* __restrict__ alpha, const __bf16* __restrict__ k,
-                                         const __bf16* __restrict__ q, const __bf16* __restrict__ v,
-                                         const float* __restrict__ beta, int64_t tok0, int L, int64_t tok_stride,
-                                         int64_t head_off, int head, int H, int tid) {
-  // Rows past the block's last token re-read its last row (always in bounds) and are replaced by
-  // neutral values (alpha = 1, k = q = v = 0, beta = 0) when they are consumed: no branches here.
+// The next block's inputs are loaded in three groups spread over the current block (alpha; k and q;
+// v and beta), so that no single burst fills the memory request queue and stalls the issuing wave.
+// Rows past the block's last token re-read its last row (always in bounds) and are replaced by
+// neutral values (alpha = 1, k = q = v = 0, beta = 0) when they are consumed: no branches here.
+struct RawAddr {
+  int64_t tok0;
+  int L;
+};
+
+__device__ __forceinline__ void load_raw_alpha(RawBlock& r, const float* __restrict__ alpha, RawAddr a,
+                                               int64_t tok_stride, int64_t head_off, int tid) {
   const int cq = tid & 31, oc = tid >> 5;
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
-    const int t = min(8 * oc + i, L - 1);
-    const int64_t base = (tok0 + t) * tok_stride + head_off + 4 * cq;
-    r.a[i] = *reinterpret_cast<const float4*>(alpha + base);
+    const int t = min(8 * oc + i, a.L - 1);
+    r.a[i] = *reinterpret_cast<const float4*>(alpha + (a.tok0 + t) * tok_stride + head_off + 4 * cq);
+  }
+}
+
+__device__ __forceinline__ void load_raw_kq(RawBlock& r, const __bf16* __restrict__ k, const __bf16* __restrict__ q,
+                                            RawAddr a, int64_t tok_stride, int64_t head_off, int tid) {
+  const int cq = tid & 31, oc = tid >> 5;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int t = min(8 * oc + i, a.L - 1);
+    const int64_t base = (a.tok0 + t) * tok_stride + head_off + 4 * cq;
     r.k[i] = *reinterpret_cast<const uint2*>(k + base);
     r.q[i] = *reinterpret_cast<const uint2*>(q + base);
   }
-  const int tv = min(tid >> 2, L - 1), part = tid & 3;
-  const uint4* src = reinterpret_cast<const uint4*>(v + (tok0 + tv) * tok_stride + head_off + 32 * part);
+}
+
+__device__ __forceinline__ void load_raw_vb(RawBlock& r, const __bf16* __restrict__ v, const float* __restrict__ beta,
+                                            RawAddr a, int64_t tok_stride, int64_t head_off, int head, int H, int tid) {
+  const int tv = min(tid >> 2, a.L - 1), part = tid & 3;
+  const uint4* src = reinterpret_cast<const uint4*>(v + (a.tok0 + tv) * tok_stride + head_off + 32 * part);
 #pragma unroll
   for (int u = 0; u < 4; ++u) r.v[u] = src[u];
-  r.b = beta[(tok0 + min(tid, L - 1)) * H + head];
+  r.b = beta[(a.tok0 + min(tid, a.L - 1)) * H + head];
 }
 
 __global__ __launch_bounds__(256, 1) void kda_prefill_kernel(KdaDevPlan p, const __bf16* __restrict__ q,
@@ -196,7 +214,12 @@ __global__ __launch_bounds__(256, 1) void kda_prefill_kernel(KdaDevPlan p, const
   }
 
   RawBlock raw;
-  load_raw(raw, alpha, k, q, v, beta, it.cu, min(kC, it.len), tok_stride, head_off, head, H, tid);
+  {
+    const RawAddr first{int64_t(it.cu), min(kC, it.len)};
+    load_raw_alpha(raw, alpha, first, tok_stride, head_off, tid);
+    load_raw_kq(raw, k, q, first, tok_stride, head_off, tid);
+    load_raw_vb(raw, v, beta, first, tok_stride, head_off, head, H, tid);
+  }
 
   for (int blk = 0; blk < it.len; blk += kC) {
     const int L = min(kC, it.len - blk);
@@ -308,12 +331,13 @@ __global__ __launch_bounds__(256, 1) void kda_prefill_kernel(KdaDevPlan p, const
           if (slow[e]) ls.slow_list[idx++] = 4 * cq + e;
       }
     }
-    // prefetch the next block's inputs; they arrive while this block is computed
-    if (blk + kC < it.len)
-      load_raw(raw, alpha, k, q, v, beta, tok0 + kC, min(kC, it.len - blk - kC), tok_stride, head_off, head, H, tid);
     lds_barrier();
 
     // ================= phase 1: A and P (waves 0-2: tiles (0,0), (1,0), (1,1)) ====================
+    // the next block's inputs arrive while this block is computed (first group here)
+    const bool more = blk + kC < it.len;
+    const RawAddr next{tok0 + kC, min(kC, it.len - blk - kC)};
+    if (more) load_raw_alpha(raw, alpha, next, tok_stride, head_off, tid);
     const int tb1 = wave == 0 ? 0 : 1, sb1 = wave == 2 ? 1 : 0;
     f32x16 accA = {}, accP = {};
     if (wave < 3) {
@@ -398,6 +422,7 @@ __global__ __launch_bounds__(256, 1) void kda_prefill_kernel(KdaDevPlan p, const
     lds_barrier();
 
     // ================= phase 2: T = (I + A)^-1 ==================================================
+    if (more) load_raw_kq(raw, k, q, next, tok_stride, head_off, tid);
     {
       // diagonal 16 x 16 blocks by forward substitution: wave -> block, lane -> column
       const int a0 = 16 * wave, jc = lane & 15;
@@ -484,6 +509,7 @@ __global__ __launch_bounds__(256, 1) void kda_prefill_kernel(KdaDevPlan p, const
     lds_barrier();
 
     // ================= phase 3: the state chain (wave -> 32 state columns) =======================
+    if (more) load_raw_vb(raw, v, beta, next, tok_stride, head_off, head, H, tid);
     {
       bf16x8 sB[4][2];
 #pragma unroll
@@ -598,6 +624,7 @@ __global__ __launch_bounds__(256, 1) void kda_prefill_kernel(KdaDevPlan p, const
       }
   }
 }
+
 
 }  // namespace
 

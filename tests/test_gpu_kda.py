@@ -112,3 +112,40 @@ def test_kda_short_chunks_sampled_heads():
 
 def test_kda_long_chunk_sampled_head():
     check_wave(wk.long(), seed=109, heads=[7])
+
+
+def _check_custom(spec, t, what):
+    g = _harness.gpu_kda(spec, t)
+    o_ref, pool_ref = _harness.oracle_kda(spec, t)
+    _compare.assert_kda_parity(g["out"].float().cpu().numpy(), o_ref, f"{what} out")
+    pool = g["state_pool"].cpu().numpy()
+    for s in _written(spec):
+        _compare.assert_kda_parity(pool[s], pool_ref[s], f"{what} slot {s}")
+
+
+@pytest.mark.parametrize("case", ["no_decay", "reset_every_token", "no_write", "unit_write"])
+def test_kda_degenerate_gates(case):
+    """alpha = 1 (no forgetting), alpha = 0 (every channel resets every token: the exact path for all
+    channels), beta = 0 (no writes: the output is the decayed snapshot read out), beta = 1."""
+    spec = wk.custom(2, 128, 128, [150, 64], [0, -1], [2, 1], 3)
+    t = wk.make_tensors(spec, seed=110)
+    if case == "no_decay":
+        t["alpha"].fill_(1.0)
+    elif case == "reset_every_token":
+        t["alpha"].fill_(0.0)
+    elif case == "no_write":
+        t["beta"].fill_(0.0)
+    else:
+        t["beta"].fill_(1.0)
+    _check_custom(spec, t, case)
+
+
+def test_kda_many_single_token_requests():
+    R = 64
+    spec = wk.custom(4, 128, 128, [1] * R, [i if i % 2 else -1 for i in range(R)], [R + i for i in range(R)], 2 * R)
+    _check_custom(spec, wk.make_tensors(spec, seed=111), "single tokens")
+
+
+def test_kda_many_heads():
+    spec = wk.custom(96, 128, 128, [70, 5], [-1, 1], [0, 2], 3)
+    _check_custom(spec, wk.make_tensors(spec, seed=112), "96 heads")

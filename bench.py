@@ -28,7 +28,9 @@ gallop/bisect prefix probe against a sharded index holding 64 such cached prompt
 stress shape), with the plain scan and the reference as comparisons.
 """
 import argparse
+import gc
 import json
+import math
 import os
 import sys
 import time
@@ -43,6 +45,40 @@ PEAK_BF16_TFLOPS = 2516.6     # 256 CU x 2.4 GHz x 4096 dense bf16 FLOP/clk/CU
 PEAK_HBM_GBS = 8000.0
 RIDGE_FLOP_PER_BYTE = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)     # ~315 FLOP/B
 METRIC = "chunked-prefill attention TFLOP/s + new tokens/s on 1 GPU; % of bf16 MFMA peak"
+
+
+def run_timed(step, sync, warmup=None, steps=None):
+    """Warm up, then time exactly `steps` steps between two device synchronizations, with Python's
+    garbage collector off (a collection pauses the host for tens of ms, and the idle GPU drops its
+    clock).  warmup None: untimed steps until at least 0.3 s and either 300 steps or 2 s have passed
+    (the runtime's one-time pool growth and the clock ramp fall inside it).  steps None: about one
+    second of timed work, 3 to 2000 steps.  Returns (warmup, steps, elapsed seconds)."""
+    t0 = time.perf_counter()
+    done = 0
+    while True:
+        if warmup is not None and done >= warmup:
+            break
+        el = time.perf_counter() - t0
+        if warmup is None and done >= 2 and el >= 0.3 and (done >= 300 or el >= 2.0):
+            break
+        step()
+        done += 1
+    sync()
+    if steps is None:
+        per = (time.perf_counter() - t0) / max(done, 1)
+        steps = int(min(2000, max(3, math.ceil(1.0 / max(per, 1e-6)))))
+    gc.collect()
+    gc.disable()
+    try:
+        sync()
+        t1 = time.perf_counter()
+        for _ in range(steps):
+            step(record=True)
+        sync()
+        elapsed = time.perf_counter() - t1
+    finally:
+        gc.enable()
+    return done, steps, elapsed
 
 
 def flops_alg(spec) -> float:
@@ -123,8 +159,9 @@ def cpu_baseline(spec, tensors, budget_s=12.0):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=None, help="timed steps (default: about one second of work)")
+    ap.add_argument("--warmup", type=int, default=None,
+                    help="untimed steps first (default: at least 0.3 s, and 300 steps or 2 s)")
     ap.add_argument("--config", default="2")
     ap.add_argument("--max-splits", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -199,15 +236,8 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step(record=True)
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    ms_per_step = elapsed * 1e3 / args.steps
+    warmup, steps, elapsed = run_timed(step, torch.cuda.synchronize, args.warmup, args.steps)
+    ms_per_step = elapsed * 1e3 / steps
     attn_ms = float(np.mean([a.elapsed_time(b) for a, b in attn_events]))
 
     # append alone, for its HBM rate (outside the timed region)
@@ -250,8 +280,8 @@ def main():
         "value": round(value, 3),
         "unit": "TFLOP/s",
         "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
+        "steps": steps,
+        "warmup": warmup,
         "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": True,
         "scaling": "weak",
@@ -367,15 +397,8 @@ def main_kda(args):
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step(record=True)
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    ms_per_step = elapsed * 1e3 / args.steps
+    warmup, steps, elapsed = run_timed(step, torch.cuda.synchronize, args.warmup, args.steps)
+    ms_per_step = elapsed * 1e3 / steps
     kms = float(np.mean([a.elapsed_time(b) for a, b in kev]))
     b = kda_bytes_alg(spec)
     f = kda_flops_alg(spec)
@@ -394,8 +417,8 @@ def main_kda(args):
         "value": round(T / (ms_per_step * 1e-3), 1),
         "unit": "tokens/s",
         "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
+        "steps": steps,
+        "warmup": warmup,
         "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": True,
         "scaling": "weak",
@@ -464,8 +487,9 @@ def main_mpu(args):
     import paper_2609_35263_amd as wp
     import oracle.mpu as omp
     wp.load_library()
-    reps = max(1, args.steps)
-    for _ in range(args.warmup):
+    reps = max(1, 20 if args.steps is None else args.steps)
+    warm = 3 if args.warmup is None else args.warmup
+    for _ in range(warm):
         mpu_trace(wp.MpuPlanner(**MPU_CONFIG), n_requests=64)
     t0 = time.perf_counter()
     dec = spent = 0
@@ -480,7 +504,7 @@ def main_mpu(args):
         "unit": "decisions/s",
         "n_gpus": 1,
         "steps": reps,
-        "warmup": args.warmup,
+        "warmup": warm,
         "ms_per_step": round(elapsed * 1e3 / reps, 3),
         "higher_is_better": True,
         "scaling": "weak",
@@ -532,9 +556,10 @@ def main_hints(args, n_req=64, prompt=200_000, block=64, seed=9100):
         _, keys = wp.block_hashes(seq, block)
         t_hash.append(time.perf_counter() - t0)
         reqs.append(keys)
-    reps = max(1, args.steps)
+    reps = max(1, 20 if args.steps is None else args.steps)
+    warm = 3 if args.warmup is None else args.warmup
     gal, lin, probes_g, probes_l = [], [], [], []
-    for _ in range(args.warmup):
+    for _ in range(warm):
         for k in reqs:
             idx.probe_prefix(0, k)
     for _ in range(reps):
@@ -555,7 +580,7 @@ def main_hints(args, n_req=64, prompt=200_000, block=64, seed=9100):
         "unit": "us",
         "n_gpus": 1,
         "steps": reps,
-        "warmup": args.warmup,
+        "warmup": warm,
         "ms_per_step": round(float(np.sum(gal)) * 1e3 / reps, 3),
         "higher_is_better": False,
         "scaling": "weak",

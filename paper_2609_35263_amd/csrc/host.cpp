@@ -100,7 +100,8 @@ double item_cost(const WorkItem& it, int G) {
 // round-robin to the kNumXcd domains, so item index k*kNumXcd + x runs on domain x.  Items of one
 // (request, KV head) read the same K/V pages; keeping them on one domain lets its L2 serve the
 // re-reads.  With few such streams, balance wins and items are placed individually.
-std::vector<WorkItem> order_items(std::vector<WorkItem> items, int G, bool xcd_aware) {
+// WAVEPP_STREAM_MAJOR=0 keeps each domain's items in plain heaviest-first order.
+std::vector<WorkItem> order_items(std::vector<WorkItem> items, int G, bool xcd_aware, bool stream_major) {
   std::vector<double> cost(items.size());
   for (size_t i = 0; i < items.size(); ++i) cost[i] = item_cost(items[i], G);
   std::vector<size_t> idx(items.size());
@@ -138,7 +139,16 @@ std::vector<WorkItem> order_items(std::vector<WorkItem> items, int G, bool xcd_a
       where[s] = x;
       load[x] += scost[s];
     }
-    for (size_t i : idx) lists[where[std::lower_bound(uniq.begin(), uniq.end(), keys[i]) - uniq.begin()]].push_back(i);
+    if (stream_major) {
+      // inside a domain, stream by stream (heaviest stream first), each stream's items heaviest
+      // first: the items running together on the domain's CUs then mostly belong to one stream and
+      // read its tiles at about the same time, so the domain's L2 serves the re-reads
+      std::vector<std::vector<size_t>> by(uniq.size());
+      for (size_t i : idx) by[std::lower_bound(uniq.begin(), uniq.end(), keys[i]) - uniq.begin()].push_back(i);
+      for (size_t s : sidx) lists[where[s]].insert(lists[where[s]].end(), by[s].begin(), by[s].end());
+    } else {
+      for (size_t i : idx) lists[where[std::lower_bound(uniq.begin(), uniq.end(), keys[i]) - uniq.begin()]].push_back(i);
+    }
   } else {
     for (size_t i : idx) {
       int x = int(std::min_element(load.begin(), load.end()) - load.begin());
@@ -434,7 +444,8 @@ int wavepp_attn_plan(const wavepp_attn_shape* shape, const wavepp_batch* batch, 
   plan->num_real_items = int32_t(items.size());
   plan->max_splits_used = max_used;
   plan->partial_rows = part_rows;
-  plan->items = order_items(std::move(items), G, env_flag("WAVEPP_XCD_ORDER", true));
+  plan->items = order_items(std::move(items), G, env_flag("WAVEPP_XCD_ORDER", true),
+                            env_flag("WAVEPP_STREAM_MAJOR", true));
   if (plan->items.size() > size_t(INT32_MAX / 2)) {
     delete plan;
     return set_error(WAVEPP_EINVAL, "too many work items");

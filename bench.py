@@ -266,6 +266,9 @@ def main():
             traffic = None
     b_layer = bytes_alg(spec)
     kernel_name = "attn_gqa_kernel" if not spec.kv_shared else "attn_mla_kernel"
+    if info.get("num_merge_items", 0) > 0:
+        # key-range splits: the timed interval (one chunked_prefill call) also holds the merge kernel
+        kernel_name += " + merge_kernel"
     if f_layer / b_layer >= RIDGE_FLOP_PER_BYTE:
         roofline = {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic, "kernel": kernel_name,

@@ -50,22 +50,37 @@ METRIC = "chunked-prefill attention TFLOP/s + new tokens/s on 1 GPU; % of bf16 M
 def run_timed(step, sync, warmup=None, steps=None):
     """Warm up, then time exactly `steps` steps between two device synchronizations, with Python's
     garbage collector off (a collection pauses the host for tens of ms, and the idle GPU drops its
-    clock).  warmup None: untimed steps until at least 0.3 s and either 300 steps or 2 s have passed
-    (the runtime's one-time pool growth and the clock ramp fall inside it).  steps None: about one
-    second of timed work, 3 to 2000 steps.  Returns (warmup, steps, elapsed seconds)."""
-    t0 = time.perf_counter()
+    clock).  The first three steps run synchronized, and the last two of them give the step time t.
+    warmup None: untimed steps for max(0.3 s, min(2 s, 300 t)) in all, so that the runtime's one-time
+    pool growth and the clock ramp fall inside them.  steps None: about one second of timed work,
+    3 to 2000 steps.  Returns (warmup, steps, elapsed seconds)."""
+    first = 3 if warmup is None else min(3, warmup)
     done = 0
-    while True:
-        if warmup is not None and done >= warmup:
-            break
-        el = time.perf_counter() - t0
-        if warmup is None and done >= 2 and el >= 0.3 and (done >= 300 or el >= 2.0):
-            break
+    t_pair = None
+    for k in range(first):
+        if k == 1:
+            sync()
+            t_pair = time.perf_counter()
+        step()
+        done += 1
+        sync()
+    per = (time.perf_counter() - t_pair) / (done - 1) if done >= 2 else None
+    if warmup is None:
+        target = max(0.3, min(2.0, 300 * per))
+        extra = max(0, math.ceil(target / per) - done)
+    else:
+        extra = warmup - done
+    for _ in range(extra):
         step()
         done += 1
     sync()
     if steps is None:
-        per = (time.perf_counter() - t0) / max(done, 1)
+        if per is None:
+            t0 = time.perf_counter()
+            step()
+            sync()
+            per = time.perf_counter() - t0
+            done += 1
         steps = int(min(2000, max(3, math.ceil(1.0 / max(per, 1e-6)))))
     gc.collect()
     gc.disable()
@@ -161,7 +176,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=None, help="timed steps (default: about one second of work)")
     ap.add_argument("--warmup", type=int, default=None,
-                    help="untimed steps first (default: at least 0.3 s, and 300 steps or 2 s)")
+                    help="untimed steps first (default: max(0.3 s, min(2 s, 300 steps)))")
     ap.add_argument("--config", default="2")
     ap.add_argument("--max-splits", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -238,7 +253,8 @@ def main():
         del src, dst
     warmup, steps, elapsed = run_timed(step, torch.cuda.synchronize, args.warmup, args.steps)
     ms_per_step = elapsed * 1e3 / steps
-    attn_ms = float(np.mean([a.elapsed_time(b) for a, b in attn_events]))
+    attn_all = [a.elapsed_time(b) for a, b in attn_events]
+    attn_ms = float(np.mean(attn_all))
 
     # append alone, for its HBM rate (outside the timed region)
     wp.plan_upload(p0, ws)
@@ -255,15 +271,16 @@ def main():
     f_step = f_layer * layers
     value = f_step / (ms_per_step * 1e-3) / 1e12
     achieved = f_layer / (attn_ms * 1e-3) / 1e12
-    traffic = None
+    traffic, counters = None, {}
     tfile = os.path.join(ROOT, "profiles", f"traffic_{spec.name}.json")
     if os.path.exists(tfile):
         try:
             tj = json.load(open(tfile))
             if tj.get("kernel_source_hash") == _kernel_hash():
                 traffic = tj.get("bytes_per_launch")
+                counters = {k: round(tj[k], 1) for k in ("mfma_util_pct", "l2_hit_pct") if k in tj}
         except Exception:
-            traffic = None
+            traffic, counters = None, {}
     b_layer = bytes_alg(spec)
     kernel_name = "attn_gqa_kernel" if not spec.kv_shared else "attn_mla_kernel"
     if info.get("num_merge_items", 0) > 0:
@@ -272,12 +289,12 @@ def main():
     if f_layer / b_layer >= RIDGE_FLOP_PER_BYTE:
         roofline = {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic, "kernel": kernel_name,
-                    "alg_flop_per_launch": f_layer, "alg_bytes_per_launch": b_layer}
+                    "alg_flop_per_launch": f_layer, "alg_bytes_per_launch": b_layer, **counters}
     else:
         gbps = b_layer / (attn_ms * 1e-3) / 1e9
         roofline = {"bound": "hbm", "achieved": round(gbps, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                     "frac": round(gbps / PEAK_HBM_GBS, 4), "traffic": traffic, "kernel": kernel_name,
-                    "alg_flop_per_launch": f_layer, "alg_bytes_per_launch": b_layer}
+                    "alg_flop_per_launch": f_layer, "alg_bytes_per_launch": b_layer, **counters}
     res = {
         "metric": METRIC,
         "value": round(value, 3),
@@ -301,6 +318,7 @@ def main():
         "new_tokens_per_s": round(T * layers / (ms_per_step * 1e-3) / layers, 1),
         "pct_peak": round(100.0 * value / PEAK_BF16_TFLOPS, 2),
         "attn_kernel_ms": round(attn_ms, 4),
+        "attn_kernel_ms_median": round(float(np.median(attn_all)), 4),
         "append_ms": round(append_ms, 4),
         "append_GBps": round(append_bytes(spec) / (append_ms * 1e-3) / 1e9, 1),
         "attn_alg_GBps": round(bytes_alg(spec) / (attn_ms * 1e-3) / 1e9, 1),
@@ -406,15 +424,16 @@ def main_kda(args):
     b = kda_bytes_alg(spec)
     f = kda_flops_alg(spec)
     gbps = b / (kms * 1e-3) / 1e9
-    traffic = None
+    traffic, counters = None, {}
     tfile = os.path.join(ROOT, "profiles", f"traffic_{spec.name}.json")
     if os.path.exists(tfile):
         try:
             tj = json.load(open(tfile))
             if tj.get("kernel_source_hash") == _kernel_hash("kda"):
                 traffic = tj.get("bytes_per_launch")
+                counters = {k: round(tj[k], 1) for k in ("mfma_util_pct", "l2_hit_pct") if k in tj}
         except Exception:
-            traffic = None
+            traffic, counters = None, {}
     res = {
         "metric": KDA_METRIC,
         "value": round(T / (ms_per_step * 1e-3), 1),
@@ -439,7 +458,7 @@ def main_kda(args):
         "work_groups": int(p0.info()["num_items"]) * spec.num_heads,
         "roofline": {"bound": "hbm", "achieved": round(gbps, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": round(gbps / PEAK_HBM_GBS, 4), "traffic": traffic, "kernel": "kda_prefill_kernel",
-                     "alg_bytes_per_launch": b, "alg_flop_per_launch": f},
+                     "alg_bytes_per_launch": b, "alg_flop_per_launch": f, **counters},
     }
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = kda_cpu_baseline(spec, wk.make_tensors(spec, seed=8000, device=dev, poison=False))
@@ -619,47 +638,66 @@ def main_hints(args, n_req=64, prompt=200_000, block=64, seed=9100):
     print(json.dumps(res), flush=True)
 
 
-def measure_traffic(config, out_json, calib_mib=1024):
-    """Two rocprofv3 counter passes (FETCH_SIZE, then WRITE_SIZE) over a short run of this config.
-
-    Each counter is scaled by what it reads for one plain device copy of calib_mib MiB in the same
-    process (known bytes / counted bytes), then averaged over the attention launches.  The GPU is
-    not touched by this process itself: the profiled runs are child processes.
-    """
+def _pmc_pass(counters, config, calib_mib):
+    """One rocprofv3 counter pass over a short child run of this config; returns the CSV rows."""
     import csv
     import subprocess
     import tempfile
+    d = tempfile.mkdtemp(prefix=f"wavepp_{counters[0].lower()}_", dir=os.environ.get("TMPDIR", "/tmp"))
+    cmd = ["rocprofv3", "--pmc", *counters, "-f", "csv", "-d", d, "-o", "run", "--",
+           sys.executable, os.path.abspath(__file__), "--config", str(config), "--steps", "2", "--warmup", "1",
+           "--no-cpu-baseline", "--copy-calibration-mib", str(calib_mib)]
+    print("[traffic] " + " ".join(cmd), flush=True)
+    res = subprocess.run(cmd, cwd=os.environ.get("TMPDIR", "/tmp"), timeout=300)
+    rows = []
+    for root, _, files in os.walk(d):
+        for f in files:
+            if f.endswith("counter_collection.csv"):
+                rows += list(csv.DictReader(open(os.path.join(root, f))))
+    if not rows:
+        print(f"[traffic] no counter rows for {counters} (rc={res.returncode})", file=sys.stderr)
+    return rows
+
+
+def measure_traffic(config, out_json, calib_mib=1024):
+    """rocprofv3 counter passes over a short run of this config: FETCH_SIZE, then WRITE_SIZE (HBM
+    bytes), then MfmaUtil, then TCC_HIT_sum and TCC_MISS_sum (L2 hit rate).
+
+    Each byte counter is scaled by what it reads for one plain device copy of calib_mib MiB in the
+    same process (known bytes / counted bytes), then averaged over the kernel's launches.  The GPU is
+    not touched by this process itself: the profiled runs are child processes.
+    """
     kind = "kda" if str(config).startswith("kda") else "attn"
     kname = "kda_prefill" if kind == "kda" else "attn_"
     out = {"config": str(config), "kernel_source_hash": _kernel_hash(kind), "calibration_copy_mib": calib_mib}
     known_kib = calib_mib * 1024.0
     for counter in ("FETCH_SIZE", "WRITE_SIZE"):
-        d = tempfile.mkdtemp(prefix=f"wavepp_{counter.lower()}_", dir=os.environ.get("TMPDIR", "/tmp"))
-        cmd = ["rocprofv3", "--pmc", counter, "-f", "csv", "-d", d, "-o", "run", "--",
-               sys.executable, os.path.abspath(__file__), "--config", str(config), "--steps", "2", "--warmup", "1",
-               "--no-cpu-baseline", "--copy-calibration-mib", str(calib_mib)]
-        print("[traffic] " + " ".join(cmd), flush=True)
-        res = subprocess.run(cmd, cwd=os.environ.get("TMPDIR", "/tmp"), timeout=300)
-        rows = []
-        for root, _, files in os.walk(d):
-            for f in files:
-                if f.endswith("counter_collection.csv"):
-                    rows += list(csv.DictReader(open(os.path.join(root, f))))
+        rows = _pmc_pass([counter], config, calib_mib)
         if not rows:
-            print(f"[traffic] no counter rows (rc={res.returncode})", file=sys.stderr)
             return 1
-        attn = [float(r["Counter_Value"]) for r in rows if kname in r["Kernel_Name"]]
+        vals = [float(r["Counter_Value"]) for r in rows if kname in r["Kernel_Name"]]
         copy = [float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"]]
-        if not attn or not copy:
-            print("[traffic] attention or calibration copy kernel missing from the counter rows", file=sys.stderr)
+        if not vals or not copy:
+            print("[traffic] kernel or calibration copy missing from the counter rows", file=sys.stderr)
             return 1
         calib = max(copy)          # the 1 GiB calibration copy; other device copies are far smaller
         factor = known_kib / calib
-        out[counter] = {"kib_per_launch": sum(attn) / len(attn), "launches": len(attn),
+        out[counter] = {"kib_per_launch": sum(vals) / len(vals), "launches": len(vals),
                         "calibration_kib": calib, "factor": factor,
-                        "bytes_per_launch": sum(attn) / len(attn) * factor * 1024.0}
+                        "bytes_per_launch": sum(vals) / len(vals) * factor * 1024.0}
     out["bytes_per_launch"] = out["FETCH_SIZE"]["bytes_per_launch"] + out["WRITE_SIZE"]["bytes_per_launch"]
-    out["command"] = f"python bench.py --config {config} --measure-traffic {out_json}"
+    rows = _pmc_pass(["MfmaUtil"], config, calib_mib)
+    util = [float(r["Counter_Value"]) for r in rows if kname in r["Kernel_Name"] and r["Counter_Name"] == "MfmaUtil"]
+    if util:
+        out["mfma_util_pct"] = sum(util) / len(util)
+    rows = _pmc_pass(["TCC_HIT_sum", "TCC_MISS_sum"], config, calib_mib)
+    hit = sum(float(r["Counter_Value"]) for r in rows if kname in r["Kernel_Name"] and r["Counter_Name"] == "TCC_HIT_sum")
+    miss = sum(float(r["Counter_Value"]) for r in rows if kname in r["Kernel_Name"] and r["Counter_Name"] == "TCC_MISS_sum")
+    if hit + miss > 0:
+        out["l2_hit_pct"] = 100.0 * hit / (hit + miss)
+    out["command"] = (f"python bench.py --config {config} --measure-traffic <out.json>  (rocprofv3 --pmc passes "
+                      f"FETCH_SIZE; WRITE_SIZE; MfmaUtil; TCC_HIT_sum TCC_MISS_sum, each over: python3 bench.py "
+                      f"--config {config} --steps 2 --warmup 1 --no-cpu-baseline --copy-calibration-mib {calib_mib})")
     with open(out_json, "w") as f:
         json.dump(out, f, indent=1)
     print(json.dumps(out), flush=True)

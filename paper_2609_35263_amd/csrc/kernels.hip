@@ -640,19 +640,50 @@ __global__ __launch_bounds__(256) void merge_kernel(DevPlan p, __bf16* __restric
   if (lrow >= mi.rows) return;
   const ReqMeta rm = p.reqs[mi.req];
   const int Hq = p.num_q_heads, G = Hq / p.num_kv_heads;
+  // Partials are read four splits at a time, so that their loads are in flight together; the
+  // accumulation order stays s = 0, 1, ..., nsplit - 1 (deterministic).  A split that saw no key has
+  // lse = -inf and an all-zero partial row, which gets weight 0.
+  const int ns = mi.nsplit;
+  const float* __restrict__ lp = p.lpart + mi.part + lrow;
+  const float* __restrict__ op = p.opart + (int64_t(mi.part) + lrow) * DV + 4 * c4;
+  const int64_t ostep = int64_t(mi.rows) * DV;
   float mx = -INFINITY;
-  for (int s = 0; s < mi.nsplit; ++s) mx = fmaxf(mx, p.lpart[mi.part + s * mi.rows + lrow]);
+  {
+    int s = 0;
+    for (; s + 4 <= ns; s += 4) {
+      float l[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) l[u] = lp[(s + u) * mi.rows];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) mx = fmaxf(mx, l[u]);
+    }
+    for (; s < ns; ++s) mx = fmaxf(mx, lp[s * mi.rows]);
+  }
   f32x4 acc = f32x4{};
   float wsum = 0.0f;
-  for (int s = 0; s < mi.nsplit; ++s) {
-    const int prow = mi.part + s * mi.rows + lrow;
-    const float l = p.lpart[prow];
-    const float w = (l == -INFINITY) ? 0.0f : fast_exp2((l - mx) * kLog2e);
-    if (w != 0.0f) {
-      const f32x4 v = *reinterpret_cast<const f32x4*>(p.opart + int64_t(prow) * DV + 4 * c4);
-      acc += w * v;
+  {
+    int s = 0;
+    for (; s + 4 <= ns; s += 4) {
+      float l[4];
+      f32x4 v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        l[u] = lp[(s + u) * mi.rows];
+        v[u] = *reinterpret_cast<const f32x4*>(op + (s + u) * ostep);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const float w = (l[u] == -INFINITY) ? 0.0f : fast_exp2((l[u] - mx) * kLog2e);
+        acc += w * v[u];
+        wsum += w;
+      }
     }
-    wsum += w;
+    for (; s < ns; ++s) {
+      const float l = lp[s * mi.rows];
+      const float w = (l == -INFINITY) ? 0.0f : fast_exp2((l - mx) * kLog2e);
+      acc += w * *reinterpret_cast<const f32x4*>(op + s * ostep);
+      wsum += w;
+    }
   }
   const float inv = 1.0f / wsum;
   const int row = mi.row0 + lrow;

@@ -46,23 +46,30 @@ typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 constexpr int kC = kKdaBlock;       // tokens per block
 constexpr int kD = kKdaDim;         // d_k = d_v
-constexpr int RS = kD + 8;          // bf16 row stride of token-major [t][channel] arrays
-constexpr int CS = kC + 8;          // bf16 row stride of [channel][t] arrays and of P, T [t][s]
+// LDS row strides.  The LDS has 64 banks of 4 bytes.  A permuted A-operand read (lds_a_perm) has the
+// 32 lanes of a half-wave read 8 bytes each from 32 consecutive rows: with a row stride that is an odd
+// multiple of 8 bytes modulo 256 those land on 32 distinct bank pairs.  Arrays read that way keep
+// rows only 8-byte aligned and are accessed 8 bytes at a time.
+constexpr int RS = kD + 8;          // bf16 row stride of K_R and of the staged output (16-byte accesses)
+constexpr int QS = kD + 4;          // bf16 row stride of Q~ and K~: 264 B
+constexpr int VS = kD + 32;         // bf16 row stride of V: 320 B, so that the 4 rows x 64 B of a
+                                    // transposing read cover the 64 banks once
+constexpr int CS = kC + 4;          // bf16 row stride of [channel][t] arrays and of P, T [t][s]: 136 B
 constexpr int AS = kC + 4;          // fp32 row stride of A and of T during the inversion
 constexpr int kSlowBatch = 16;      // slow channels staged per pass
 constexpr float kFastFloor = 0x1p-96f;
 constexpr float kLogFloor = -1000.0f;   // log2 of a zero decay: exp2 of it is exactly 0 in fp32
 
 struct KdaLds {
-  __bf16 qt[kC * RS];               // Q~ = gamma * q          [t][c]
-  __bf16 kt[kC * RS];               // K~ = gamma * k          [t][c]
+  __bf16 qt[kC * QS];               // Q~ = gamma * q          [t][c]
+  __bf16 kt[kC * QS];               // K~ = gamma * k          [t][c]
   union {
     __bf16 kr[kC * RS];             // K_R = k / gamma (0 for slow channels)   [t][c]
     float tf[kC * AS];              // T = (I + A)^-1 in fp32 while it is built
     __bf16 ob[kC * RS];             // the block's output rows, staged for 16-byte stores
   };
   __bf16 kbt[kD * CS];              // Kbar^T                  [c][t]
-  __bf16 v[kC * RS];                // V                       [t][j]
+  __bf16 v[kC * VS];                // V                       [t][j]
   union {
     float a[kC * AS];               // A (beta-scaled, strictly lower)
     struct {                        // slow channels of one batch, log2-space
@@ -174,9 +181,11 @@ __device__ __forceinline__ void load_raw_kq(RawBlock& r, const __bf16* __restric
 __device__ __forceinline__ void load_raw_vb(RawBlock& r, const __bf16* __restrict__ v, const float* __restrict__ beta,
                                             RawAddr a, int64_t tok_stride, int64_t head_off, int head, int H, int tid) {
   const int tv = min(tid >> 2, a.L - 1), part = tid & 3;
-  const uint4* src = reinterpret_cast<const uint4*>(v + (a.tok0 + tv) * tok_stride + head_off + 32 * part);
+  // lane `part` of a row takes its 16-byte chunks part + 4u: the four lanes of a row read (and later
+  // write to LDS) 64 contiguous bytes per u
+  const uint4* src = reinterpret_cast<const uint4*>(v + (a.tok0 + tv) * tok_stride + head_off + 8 * part);
 #pragma unroll
-  for (int u = 0; u < 4; ++u) r.v[u] = src[u];
+  for (int u = 0; u < 4; ++u) r.v[u] = src[4 * u];
   r.b = beta[(a.tok0 + min(tid, a.L - 1)) * H + head];
 }
 
@@ -254,7 +263,7 @@ __global__ __launch_bounds__(256, 1) void kda_prefill_kernel(KdaDevPlan p, const
       const bool vok = tv < L;
 #pragma unroll
       for (int u = 0; u < 4; ++u)
-        *reinterpret_cast<uint4*>(&ls.v[tv * RS + 32 * part + 8 * u]) = vok ? raw.v[u] : make_uint4(0, 0, 0, 0);
+        *reinterpret_cast<uint4*>(&ls.v[tv * VS + 8 * part + 32 * u]) = vok ? raw.v[u] : make_uint4(0, 0, 0, 0);
       if (tid < kC) ls.beta[tid] = tid < L ? raw.b : 0.0f;
     }
     lds_barrier();
@@ -303,14 +312,16 @@ __global__ __launch_bounds__(256, 1) void kda_prefill_kernel(KdaDevPlan p, const
           vr[e] = static_cast<__bf16>(kbar * inv_tot[e]);
           kb[e][i] = static_cast<__bf16>(kbar);
         }
-        *reinterpret_cast<bf16x4*>(&ls.qt[t * RS + 4 * cq]) = vq;
-        *reinterpret_cast<bf16x4*>(&ls.kt[t * RS + 4 * cq]) = vk;
+        *reinterpret_cast<bf16x4*>(&ls.qt[t * QS + 4 * cq]) = vq;
+        *reinterpret_cast<bf16x4*>(&ls.kt[t * QS + 4 * cq]) = vk;
         *reinterpret_cast<bf16x4*>(&ls.kr[t * RS + 4 * cq]) = vr;
       }
 #pragma unroll
-      for (int e = 0; e < 4; ++e)
-        *reinterpret_cast<bf16x8*>(&ls.kbt[(4 * cq + e) * CS + 8 * oc]) =
-            bf16x8{kb[e][0], kb[e][1], kb[e][2], kb[e][3], kb[e][4], kb[e][5], kb[e][6], kb[e][7]};
+      for (int e = 0; e < 4; ++e) {
+        __bf16* kp = &ls.kbt[(4 * cq + e) * CS + 8 * oc];
+        *reinterpret_cast<bf16x4*>(kp) = bf16x4{kb[e][0], kb[e][1], kb[e][2], kb[e][3]};
+        *reinterpret_cast<bf16x4*>(kp + 4) = bf16x4{kb[e][4], kb[e][5], kb[e][6], kb[e][7]};
+      }
       if (oc == 0) *reinterpret_cast<float4*>(&ls.gc[4 * cq]) = make_float4(tot[0], tot[1], tot[2], tot[3]);
     }
     // compact list of the slow channels, in channel order (lanes 0-31 of every wave see all channels)
@@ -343,8 +354,10 @@ __global__ __launch_bounds__(256, 1) void kda_prefill_kernel(KdaDevPlan p, const
     if (wave < 3) {
 #pragma unroll
       for (int kc = 0; kc < kD / 16; ++kc) {
-        const bf16x8 ak = *reinterpret_cast<const bf16x8*>(&ls.kt[(32 * tb1 + col) * RS + 16 * kc + 8 * hf]);
-        const bf16x8 aq = *reinterpret_cast<const bf16x8*>(&ls.qt[(32 * tb1 + col) * RS + 16 * kc + 8 * hf]);
+        const __bf16* kp = &ls.kt[(32 * tb1 + col) * QS + 16 * kc + 8 * hf];
+        const __bf16* qp = &ls.qt[(32 * tb1 + col) * QS + 16 * kc + 8 * hf];
+        const bf16x8 ak = cat(*reinterpret_cast<const bf16x4*>(kp), *reinterpret_cast<const bf16x4*>(kp + 4));
+        const bf16x8 aq = cat(*reinterpret_cast<const bf16x4*>(qp), *reinterpret_cast<const bf16x4*>(qp + 4));
         const bf16x8 b = *reinterpret_cast<const bf16x8*>(&ls.kr[(32 * sb1 + col) * RS + 16 * kc + 8 * hf]);
         accA = mfma(ak, b, accA);
         accP = mfma(aq, b, accP);
@@ -503,7 +516,8 @@ __global__ __launch_bounds__(256, 1) void kda_prefill_kernel(KdaDevPlan p, const
         bf16x8 w;
 #pragma unroll
         for (int e = 0; e < 8; ++e) w[e] = static_cast<__bf16>(((s0 + e) >> 4) <= (t >> 4) ? ls.tf[t * AS + s0 + e] : 0.0f);
-        *reinterpret_cast<bf16x8*>(&ls.tm[t * CS + s0]) = w;
+        *reinterpret_cast<bf16x4*>(&ls.tm[t * CS + s0]) = bf16x4{w[0], w[1], w[2], w[3]};
+        *reinterpret_cast<bf16x4*>(&ls.tm[t * CS + s0 + 4]) = bf16x4{w[4], w[5], w[6], w[7]};
       }
     }
     lds_barrier();
@@ -525,8 +539,8 @@ __global__ __launch_bounds__(256, 1) void kda_prefill_kernel(KdaDevPlan p, const
 #pragma unroll
           for (int tb = 0; tb < 2; ++tb) {
             const int cb = 32 * ib + 16 * kk + 4 * hf;
-            accE[tb] = mfma(lds_a_perm(&ls.kt[(32 * tb + col) * RS], cb), sB[ib][kk], accE[tb]);
-            accO[tb] = mfma(lds_a_perm(&ls.qt[(32 * tb + col) * RS], cb), sB[ib][kk], accO[tb]);
+            accE[tb] = mfma(lds_a_perm(&ls.kt[(32 * tb + col) * QS], cb), sB[ib][kk], accE[tb]);
+            accO[tb] = mfma(lds_a_perm(&ls.qt[(32 * tb + col) * QS], cb), sB[ib][kk], accO[tb]);
           }
       // R = beta (V - E), in place in accE.  V[t0 + r][j] for r = 0..3 comes from the transposing
       // read: lane 4m + g of each 16-lane group addresses row t0 + m at column 4g of its group.
@@ -538,7 +552,7 @@ __global__ __launch_bounds__(256, 1) void kda_prefill_kernel(KdaDevPlan p, const
 #pragma unroll
         for (int b = 0; b < 4; ++b) {
           const int t0 = 32 * tb + 8 * b + 4 * hf;
-          const bf16x4 vv = lds_read_tr(&ls.v[(t0 + (li >> 2)) * RS + jg]);
+          const bf16x4 vv = lds_read_tr(&ls.v[(t0 + (li >> 2)) * VS + jg]);
           const float4 bt = *reinterpret_cast<const float4*>(&ls.beta[t0]);
           const float bs[4] = {bt.x, bt.y, bt.z, bt.w};
 #pragma unroll

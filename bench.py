@@ -26,6 +26,11 @@ trace shaped like the paper's eight-stage runs), against the reference planner a
 times reuse-hint discovery on the host: chained block hashing of 200K-token requests and the
 gallop/bisect prefix probe against a sharded index holding 64 such cached prompts (the paper's
 stress shape), with the plain scan and the reference as comparisons.
+
+    python bench.py --config peak
+
+measures what the matrix cores sustain on this GPU (a register-only MFMA probe) and the shader clock
+meanwhile, the reference point beside the nominal 2516.6 TFLOP/s.
 """
 import argparse
 import gc
@@ -198,6 +203,8 @@ def main():
         return main_mpu(args)
     if str(args.config) == "hints":
         return main_hints(args)
+    if str(args.config) == "peak":
+        return main_peak(args)
 
     import numpy as np
     import torch
@@ -467,6 +474,66 @@ def main_kda(args):
 
 MPU_CONFIG = dict(max_budget=16384, min_budget=8192, block=64, stages=8, fills=1, max_lanes=64,
                   count_inflight=False)
+
+
+def main_peak(args, workgroups=1024, iters=20000):
+    """The dense bf16 matrix-core rate the chip sustains, and its shader clock meanwhile: the probe
+    kernel of wavepp_probe.h (register operands only, four independent MFMA chains per wave)."""
+    import ctypes
+    import torch
+    import paper_2609_35263_amd as wp
+    lib = wp.load_library()
+    lib.wavepp_probe_mfma.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+                                      ctypes.c_void_p]
+    lib.wavepp_probe_mfma.restype = ctypes.c_int
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    sink = torch.empty(workgroups * 512, dtype=torch.float32, device=dev)
+    clocks = torch.zeros(4, dtype=torch.int64, device=dev)
+    stream = torch.cuda.current_stream()
+    events = []
+
+    def step(record=False):
+        if record:
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+        st = lib.wavepp_probe_mfma(workgroups, iters, ctypes.c_void_p(sink.data_ptr()),
+                                   ctypes.c_void_p(clocks.data_ptr()), ctypes.c_void_p(stream.cuda_stream))
+        if st != 0:
+            raise RuntimeError(f"probe failed: {st}")
+        if record:
+            e1.record(stream)
+            events.append((e0, e1))
+
+    warmup, steps, elapsed = run_timed(step, torch.cuda.synchronize, args.warmup, args.steps)
+    ms = float(np.median([a.elapsed_time(b) for a, b in events]))
+    flop = workgroups * 8 * iters * 4 * 32768.0
+    tflops = flop / (ms * 1e-3) / 1e12
+    c = clocks.cpu().numpy().astype(np.float64)
+    sclk_ghz = (c[2] - c[0]) / ((c[3] - c[1]) * 10.0)          # s_memrealtime ticks at 100 MHz
+    at_clk = 256 * sclk_ghz * 1e9 * 4096 / 1e12
+    res = {
+        "metric": "dense bf16 MFMA TFLOP/s sustained by a register-only probe (v_mfma_f32_32x32x16_bf16)",
+        "value": round(tflops, 1),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warmup,
+        "ms_per_step": round(elapsed * 1e3 / steps, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{workgroups} workgroups x 8 waves x {iters} rounds x 4 MFMA chains",
+                   "parallelism": "none (1 GPU)"},
+        "sclk_ghz_under_load": round(float(sclk_ghz), 3),
+        "peak_at_measured_clock": round(at_clk, 1),
+        "frac_of_nominal": round(tflops / PEAK_BF16_TFLOPS, 4),
+        "frac_at_measured_clock": round(tflops / at_clk, 4),
+        "roofline": None,
+    }
+    print(json.dumps(res), flush=True)
 
 
 def mpu_trace(planner, n_requests=512, concurrency=64, seed=9000):

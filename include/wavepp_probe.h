@@ -1,0 +1,36 @@
+/*
+ * wavepp_probe.h -- measurement probe of libwavepp_attn.so (not part of the attention path): the
+ * dense bf16 matrix-core rate and the shader clock of the GPU it runs on, so that a roofline can be
+ * quoted against what the chip actually sustains as well as against its nominal peak.
+ *
+ * The probe kernel keeps every operand in registers: each wave runs `iters` rounds of four
+ * independent v_mfma_f32_32x32x16_bf16 chains (32 x 32 x 16 x 2 = 32,768 FLOP each), then writes
+ * one float per thread to `sink` so the work is not optimized away.  Lane 0 of workgroup 0 records
+ * s_memtime (shader clock cycles) and s_memrealtime (a 100 MHz counter) before and after its loop;
+ * their ratio gives the shader clock while the matrix cores are busy.
+ *
+ * Arguments (device pointers, caller-owned):
+ *   workgroups  grid size, >= 1; each workgroup is 512 threads (8 waves)
+ *   iters       rounds per wave, >= 1
+ *   sink        float[workgroups * 512]
+ *   clocks      uint64[4]: memtime start, memrealtime start, memtime end, memrealtime end
+ * FLOP per launch = workgroups * 8 * iters * 4 * 32768.
+ * Errors: WAVEPP_EINVAL for a non-positive size or a NULL pointer; launch errors as WAVEPP_EHIP.
+ */
+#ifndef WAVEPP_PROBE_H
+#define WAVEPP_PROBE_H
+
+#include "wavepp_attn.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+int wavepp_probe_mfma(int32_t workgroups, int32_t iters, float* sink, unsigned long long* clocks,
+                      hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* WAVEPP_PROBE_H */

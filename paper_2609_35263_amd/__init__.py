@@ -49,6 +49,7 @@ KDA_SYMBOLS = [
     "wavepp_kda_plan", "wavepp_kda_workspace_bytes", "wavepp_kda_get_info", "wavepp_kda_upload",
     "wavepp_kda_chunked_prefill", "wavepp_kda_destroy",
 ]
+PROBE_SYMBOLS = ["wavepp_probe_mfma"]
 
 
 class WaveppError(RuntimeError):

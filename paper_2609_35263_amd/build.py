@@ -13,7 +13,7 @@ LIB = os.path.join(HERE, "libwavepp_attn.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = os.environ.get("WAVEPP_OFFLOAD_ARCH", "gfx950")
 
-SOURCES = ["kernels.hip", "kda.hip", "host.cpp", "kda_host.cpp", "mpu.cpp", "hints.cpp"]
+SOURCES = ["kernels.hip", "kda.hip", "probe.hip", "host.cpp", "kda_host.cpp", "mpu.cpp", "hints.cpp"]
 
 FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",

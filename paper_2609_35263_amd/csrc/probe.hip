@@ -1,0 +1,67 @@
+// Matrix-core rate and shader-clock probe (a measurement tool beside the attention path).
+#include <hip/hip_runtime.h>
+
+#include "wavepp_probe.h"
+#include "internal.h"
+
+namespace wavepp {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int kProbeThreads = 512;
+
+__global__ __launch_bounds__(kProbeThreads) void mfma_probe_kernel(int iters, float* __restrict__ sink,
+                                                                   unsigned long long* __restrict__ clocks) {
+  const int tid = threadIdx.x;
+  // operands from the thread index, so that nothing folds at compile time
+  bf16x8 a, b;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    a[e] = static_cast<__bf16>(float((tid + e) & 7) * 0.125f);
+    b[e] = static_cast<__bf16>(float((tid * 3 + e) & 7) * 0.0625f);
+  }
+  f32x16 acc[4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) acc[c] = f32x16{};
+  const bool rec = blockIdx.x == 0 && tid == 0;
+  unsigned long long t0 = 0, r0 = 0;
+  if (rec) {
+    t0 = __builtin_amdgcn_s_memtime();
+    r0 = __builtin_amdgcn_s_memrealtime();
+  }
+  for (int i = 0; i < iters; ++i) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[c], 0, 0, 0);
+  }
+  float s = 0.0f;
+#pragma unroll
+  for (int c = 0; c < 4; ++c)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) s += acc[c][r];
+  if (rec) {
+    const unsigned long long t1 = __builtin_amdgcn_s_memtime();
+    const unsigned long long r1 = __builtin_amdgcn_s_memrealtime();
+    clocks[0] = t0;
+    clocks[1] = r0;
+    clocks[2] = t1;
+    clocks[3] = r1;
+  }
+  sink[int64_t(blockIdx.x) * kProbeThreads + tid] = s;
+}
+
+}  // namespace
+}  // namespace wavepp
+
+extern "C" int wavepp_probe_mfma(int32_t workgroups, int32_t iters, float* sink, unsigned long long* clocks,
+                                 hipStream_t stream) {
+  using namespace wavepp;
+  clear_error();
+  if (workgroups <= 0 || iters <= 0) return set_error(WAVEPP_EINVAL, "workgroups and iters must be positive");
+  if (!sink || !clocks) return set_error(WAVEPP_EINVAL, "sink / clocks is NULL");
+  hipLaunchKernelGGL(mfma_probe_kernel, dim3(workgroups), dim3(kProbeThreads), 0, stream, iters, sink, clocks);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return set_hip_error(e, "probe launch");
+  return WAVEPP_OK;
+}

@@ -194,3 +194,31 @@ def test_reuse_hints_planner_and_kernels_end_to_end():
     # the reused snapshots were only read
     for b, slot in snapshots.items():
         assert all(r.slot != slot for r in reqs)
+
+
+def test_mfma_probe_reports_a_plausible_rate_and_clock():
+    """The measurement probe (wavepp_probe.h): its clock reading and its rate stay within what an
+    MI355X can do (not a performance bar: a broken probe would read zero, negative or absurd)."""
+    import ctypes
+    lib = wp.load_library()
+    lib.wavepp_probe_mfma.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+                                      ctypes.c_void_p]
+    sink = torch.empty(256 * 512, dtype=torch.float32, device="cuda")
+    clocks = torch.zeros(4, dtype=torch.int64, device="cuda")
+    s = torch.cuda.current_stream()
+    assert lib.wavepp_probe_mfma(0, 10, ctypes.c_void_p(sink.data_ptr()), ctypes.c_void_p(clocks.data_ptr()),
+                                 ctypes.c_void_p(s.cuda_stream)) == -1
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for _ in range(2):
+        e0.record(s)
+        assert lib.wavepp_probe_mfma(256, 2000, ctypes.c_void_p(sink.data_ptr()), ctypes.c_void_p(clocks.data_ptr()),
+                                     ctypes.c_void_p(s.cuda_stream)) == 0
+        e1.record(s)
+    torch.cuda.synchronize()
+    c = clocks.cpu().numpy().astype(np.float64)
+    ghz = (c[2] - c[0]) / ((c[3] - c[1]) * 10.0)
+    tflops = 256 * 8 * 2000 * 4 * 32768.0 / (e0.elapsed_time(e1) * 1e-3) / 1e12
+    print(f"[probe] {tflops:.0f} TFLOP/s at {ghz:.2f} GHz", flush=True)
+    assert 0.3 < ghz < 3.0
+    assert 50.0 < tflops < 2600.0
+    assert torch.isfinite(sink).all()

@@ -19,7 +19,8 @@ def test_library_loads_and_exports_every_declared_symbol():
             header = open(os.path.join(ROOT, "include", name)).read()
             declared |= set(re.findall(r"^(?:const\s+)?\w+\s*\*?\s*(wavepp_\w+)\s*\(", header, re.M))
     assert declared, "no declarations found"
-    assert declared == set(wp.EXPORTED_SYMBOLS) | set(wp.KDA_SYMBOLS) | set(wp.MPU_SYMBOLS) | set(wp.HINT_SYMBOLS)
+    assert declared == (set(wp.EXPORTED_SYMBOLS) | set(wp.KDA_SYMBOLS) | set(wp.MPU_SYMBOLS) | set(wp.HINT_SYMBOLS)
+                        | set(wp.PROBE_SYMBOLS))
     for name in declared:
         assert hasattr(lib, name), name
 

@@ -332,6 +332,11 @@ def main():
         "work_items": info["num_items"],
         "roofline": roofline,
     }
+    # what the matrix cores sustain on this chip with random-bit operands (a power-limited clock), as
+    # context for the nominal peak; run after the timed region
+    p_tf, p_ghz = mfma_probe(torch)
+    res["mfma_probe"] = {"tflops": round(p_tf, 1), "sclk_ghz": round(p_ghz, 3),
+                         "attn_frac_of_probe": round(achieved / p_tf, 4) if roofline["bound"] == "mfma" else None}
     if not args.no_cpu_baseline:
         # the pools were appended to in place on the device; start from the generator's output again
         fresh = cpu_layer0 if cpu_layer0 is not None else wl.make_tensors(spec, seed=seed, device=dev, poison=False)
@@ -476,6 +481,33 @@ MPU_CONFIG = dict(max_budget=16384, min_budget=8192, block=64, stages=8, fills=1
                   count_inflight=False)
 
 
+def mfma_probe(torch, workgroups=1024, iters=20000, random_ops=1, launches=20):
+    """Median TFLOP/s and shader clock (GHz) of the register-only MFMA probe over a few launches."""
+    import ctypes
+    import paper_2609_35263_amd as wp
+    lib = wp.load_library()
+    lib.wavepp_probe_mfma.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+                                      ctypes.c_void_p, ctypes.c_void_p]
+    lib.wavepp_probe_mfma.restype = ctypes.c_int
+    sink = torch.empty(workgroups * 512, dtype=torch.float32, device="cuda")
+    clocks = torch.zeros(4, dtype=torch.int64, device="cuda")
+    stream = torch.cuda.current_stream()
+    ms = []
+    for _ in range(launches):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        st = lib.wavepp_probe_mfma(workgroups, iters, random_ops, ctypes.c_void_p(sink.data_ptr()),
+                                   ctypes.c_void_p(clocks.data_ptr()), ctypes.c_void_p(stream.cuda_stream))
+        if st != 0:
+            raise RuntimeError(f"probe failed: {st}")
+        e1.record(stream)
+        ms.append((e0, e1))
+    torch.cuda.synchronize()
+    t = float(np.median([a.elapsed_time(b) for a, b in ms[len(ms) // 2:]]))
+    c = clocks.cpu().numpy().astype(np.float64)
+    return workgroups * 8 * iters * 4 * 32768.0 / (t * 1e-3) / 1e12, float((c[2] - c[0]) / ((c[3] - c[1]) * 10.0))
+
+
 def main_peak(args, workgroups=1024, iters=20000):
     """The dense bf16 matrix-core rate the chip sustains, and its shader clock meanwhile: the probe
     kernel of wavepp_probe.h (register operands only, four independent MFMA chains per wave)."""
@@ -483,8 +515,8 @@ def main_peak(args, workgroups=1024, iters=20000):
     import torch
     import paper_2609_35263_amd as wp
     lib = wp.load_library()
-    lib.wavepp_probe_mfma.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
-                                      ctypes.c_void_p]
+    lib.wavepp_probe_mfma.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+                                      ctypes.c_void_p, ctypes.c_void_p]
     lib.wavepp_probe_mfma.restype = ctypes.c_int
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
@@ -492,12 +524,13 @@ def main_peak(args, workgroups=1024, iters=20000):
     clocks = torch.zeros(4, dtype=torch.int64, device=dev)
     stream = torch.cuda.current_stream()
     events = []
+    random_ops = 1
 
     def step(record=False):
         if record:
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record(stream)
-        st = lib.wavepp_probe_mfma(workgroups, iters, ctypes.c_void_p(sink.data_ptr()),
+        st = lib.wavepp_probe_mfma(workgroups, iters, random_ops, ctypes.c_void_p(sink.data_ptr()),
                                    ctypes.c_void_p(clocks.data_ptr()), ctypes.c_void_p(stream.cuda_stream))
         if st != 0:
             raise RuntimeError(f"probe failed: {st}")
@@ -505,9 +538,17 @@ def main_peak(args, workgroups=1024, iters=20000):
             e1.record(stream)
             events.append((e0, e1))
 
+    flop = workgroups * 8 * iters * 4 * 32768.0
+    # small constant operands first (for the record), then random-bit ones (the reported value)
+    random_ops = 0
+    run_timed(step, torch.cuda.synchronize, 3, 20)
+    c = clocks.cpu().numpy().astype(np.float64)
+    quiet = {"tflops": round(flop / (float(np.median([a.elapsed_time(b) for a, b in events])) * 1e-3) / 1e12, 1),
+             "sclk_ghz": round(float((c[2] - c[0]) / ((c[3] - c[1]) * 10.0)), 3)}
+    events.clear()
+    random_ops = 1
     warmup, steps, elapsed = run_timed(step, torch.cuda.synchronize, args.warmup, args.steps)
     ms = float(np.median([a.elapsed_time(b) for a, b in events]))
-    flop = workgroups * 8 * iters * 4 * 32768.0
     tflops = flop / (ms * 1e-3) / 1e12
     c = clocks.cpu().numpy().astype(np.float64)
     sclk_ghz = (c[2] - c[0]) / ((c[3] - c[1]) * 10.0)          # s_memrealtime ticks at 100 MHz
@@ -525,8 +566,9 @@ def main_peak(args, workgroups=1024, iters=20000):
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": f"{workgroups} workgroups x 8 waves x {iters} rounds x 4 MFMA chains",
-                   "parallelism": "none (1 GPU)"},
+        "config": {"workload": f"{workgroups} workgroups x 8 waves x {iters} rounds x 4 MFMA chains, random-bit "
+                               f"bf16 operands", "parallelism": "none (1 GPU)"},
+        "small_constant_operands": quiet,
         "sclk_ghz_under_load": round(float(sclk_ghz), 3),
         "peak_at_measured_clock": round(at_clk, 1),
         "frac_of_nominal": round(tflops / PEAK_BF16_TFLOPS, 4),

@@ -12,6 +12,8 @@
  * Arguments (device pointers, caller-owned):
  *   workgroups  grid size, >= 1; each workgroup is 512 threads (8 waves)
  *   iters       rounds per wave, >= 1
+ *   random_operands  0: a few small constant operand values; 1: random-bit bf16 operands spread
+ *               like N(0,1) samples (more bits toggle, as with attention's Q/K/V, and more power)
  *   sink        float[workgroups * 512]
  *   clocks      uint64[4]: memtime start, memrealtime start, memtime end, memrealtime end
  * FLOP per launch = workgroups * 8 * iters * 4 * 32768.
@@ -26,8 +28,8 @@
 extern "C" {
 #endif
 
-int wavepp_probe_mfma(int32_t workgroups, int32_t iters, float* sink, unsigned long long* clocks,
-                      hipStream_t stream);
+int wavepp_probe_mfma(int32_t workgroups, int32_t iters, int32_t random_operands, float* sink,
+                      unsigned long long* clocks, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -12,15 +12,33 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int kProbeThreads = 512;
 
-__global__ __launch_bounds__(kProbeThreads) void mfma_probe_kernel(int iters, float* __restrict__ sink,
+__device__ __forceinline__ uint32_t mix32(uint32_t x) {   // an integer hash (xorshift-multiply)
+  x ^= x >> 16;
+  x *= 0x7feb352du;
+  x ^= x >> 15;
+  x *= 0x846ca68bu;
+  x ^= x >> 16;
+  return x;
+}
+
+__global__ __launch_bounds__(kProbeThreads) void mfma_probe_kernel(int iters, int random_operands,
+                                                                   float* __restrict__ sink,
                                                                    unsigned long long* __restrict__ clocks) {
   const int tid = threadIdx.x;
-  // operands from the thread index, so that nothing folds at compile time
+  // operands from the thread index, so that nothing folds at compile time: a few small values, or
+  // N(0,1)-like bf16 values with random mantissa bits (as attention operands have)
   bf16x8 a, b;
+  const uint32_t seed = (blockIdx.x * kProbeThreads + tid) * 16u;
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
-    a[e] = static_cast<__bf16>(float((tid + e) & 7) * 0.125f);
-    b[e] = static_cast<__bf16>(float((tid * 3 + e) & 7) * 0.0625f);
+    if (random_operands) {
+      const uint32_t ha = mix32(seed + e), hb = mix32(seed + 8 + e);
+      a[e] = static_cast<__bf16>((float(ha & 0xffffu) - 32768.0f) * (1.0f / 16384.0f));
+      b[e] = static_cast<__bf16>((float(hb & 0xffffu) - 32768.0f) * (1.0f / 16384.0f));
+    } else {
+      a[e] = static_cast<__bf16>(float((tid + e) & 7) * 0.125f);
+      b[e] = static_cast<__bf16>(float((tid * 3 + e) & 7) * 0.0625f);
+    }
   }
   f32x16 acc[4];
 #pragma unroll
@@ -54,13 +72,14 @@ __global__ __launch_bounds__(kProbeThreads) void mfma_probe_kernel(int iters, fl
 }  // namespace
 }  // namespace wavepp
 
-extern "C" int wavepp_probe_mfma(int32_t workgroups, int32_t iters, float* sink, unsigned long long* clocks,
-                                 hipStream_t stream) {
+extern "C" int wavepp_probe_mfma(int32_t workgroups, int32_t iters, int32_t random_operands, float* sink,
+                                 unsigned long long* clocks, hipStream_t stream) {
   using namespace wavepp;
   clear_error();
   if (workgroups <= 0 || iters <= 0) return set_error(WAVEPP_EINVAL, "workgroups and iters must be positive");
   if (!sink || !clocks) return set_error(WAVEPP_EINVAL, "sink / clocks is NULL");
-  hipLaunchKernelGGL(mfma_probe_kernel, dim3(workgroups), dim3(kProbeThreads), 0, stream, iters, sink, clocks);
+  hipLaunchKernelGGL(mfma_probe_kernel, dim3(workgroups), dim3(kProbeThreads), 0, stream, iters,
+                     random_operands ? 1 : 0, sink, clocks);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return set_hip_error(e, "probe launch");
   return WAVEPP_OK;

@@ -201,18 +201,18 @@ def test_mfma_probe_reports_a_plausible_rate_and_clock():
     MI355X can do (not a performance bar: a broken probe would read zero, negative or absurd)."""
     import ctypes
     lib = wp.load_library()
-    lib.wavepp_probe_mfma.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
-                                      ctypes.c_void_p]
+    lib.wavepp_probe_mfma.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+                                      ctypes.c_void_p, ctypes.c_void_p]
     sink = torch.empty(256 * 512, dtype=torch.float32, device="cuda")
     clocks = torch.zeros(4, dtype=torch.int64, device="cuda")
     s = torch.cuda.current_stream()
-    assert lib.wavepp_probe_mfma(0, 10, ctypes.c_void_p(sink.data_ptr()), ctypes.c_void_p(clocks.data_ptr()),
+    assert lib.wavepp_probe_mfma(0, 10, 1, ctypes.c_void_p(sink.data_ptr()), ctypes.c_void_p(clocks.data_ptr()),
                                  ctypes.c_void_p(s.cuda_stream)) == -1
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     for _ in range(2):
         e0.record(s)
-        assert lib.wavepp_probe_mfma(256, 2000, ctypes.c_void_p(sink.data_ptr()), ctypes.c_void_p(clocks.data_ptr()),
-                                     ctypes.c_void_p(s.cuda_stream)) == 0
+        assert lib.wavepp_probe_mfma(256, 2000, 1, ctypes.c_void_p(sink.data_ptr()),
+                                     ctypes.c_void_p(clocks.data_ptr()), ctypes.c_void_p(s.cuda_stream)) == 0
         e1.record(s)
     torch.cuda.synchronize()
     c = clocks.cpu().numpy().astype(np.float64)

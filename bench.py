@@ -813,14 +813,39 @@ def measure_traffic(config, out_json, calib_mib=1024):
     return 0
 
 
-def _kernel_hash(kind="attn"):
-    """Hash of the sources that decide a kernel's memory traffic: its kernel file, its planner and the
-    shared layout header."""
+def _code_only(text: str) -> str:
+    """C/C++ source without comments and with whitespace collapsed (string literals kept as they are)."""
+    import re
+    out, i, n = [], 0, len(text)
+    while i < n:
+        c = text[i]
+        if c == '"' or c == "'":
+            j = i + 1
+            while j < n and text[j] != c:
+                j += 2 if text[j] == "\\" else 1
+            out.append(text[i:j + 1])
+            i = j + 1
+        elif text.startswith("//", i):
+            j = text.find("\n", i)
+            i = n if j < 0 else j
+        elif text.startswith("/*", i):
+            j = text.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+        else:
+            out.append(c)
+            i += 1
+    return re.sub(r"\s+", " ", "".join(out)).strip()
+
+
+def _kernel_hash(kind="attn", read=None):
+    """Hash of the code (comments and layout ignored) that decides a kernel's memory traffic: its kernel
+    file, its planner and the shared layout header."""
     import hashlib
+    read = read or (lambda f: open(os.path.join(ROOT, "paper_2609_35263_amd", "csrc", f)).read())
     h = hashlib.sha256()
     files = ("kernels.hip", "host.cpp", "internal.h") if kind == "attn" else ("kda.hip", "kda_host.cpp", "internal.h")
     for f in files:
-        h.update(open(os.path.join(ROOT, "paper_2609_35263_amd", "csrc", f), "rb").read())
+        h.update(_code_only(read(f)).encode())
     return h.hexdigest()[:16]
 
 

@@ -2,7 +2,8 @@
 // attention over paged K/V with bf16 MFMA, and the merge of key-range splits.
 //
 // Attention layout (one workgroup = 8 waves = one work item of up to 256 query rows; one workgroup
-// per CU, two waves per SIMD):
+// per CU, two waves per SIMD.  A 4-wave form with 128-row items and 64-key tiles runs two
+// workgroups per CU for waves whose (request, KV head) pairs have at most 128 rows):
 //   * Rows are (token, head-in-group) pairs of one (request, KV head): row = token * G + h, so the
 //     G query heads that share a KV head share every K/V tile loaded into LDS.
 //   * Each wave owns 32 rows.  Logits are computed transposed, S^T = K Q^T, with
@@ -14,9 +15,10 @@
 //     of O^T += V^T P^T: the key order inside that contraction is the order in which the
 //     accumulator holds them.  V is staged in LDS row-major like K and read with gfx950's
 //     transposing LDS load (ds_read_b64_tr_b16) in that matching order.
-//   * K/V tiles of 64 keys are gathered from the pages named by the block table with 16-byte
-//     loads (one page's head slice is contiguous), double-buffered in LDS: the next tile's global
-//     loads are issued before the current tile's MFMAs and written to the other buffer after.
+//   * K/V tiles of 128 keys (64 in the 4-wave form) are gathered from the pages named by the block
+//     table with 16-byte loads (one page's head slice is contiguous), double-buffered in LDS: the
+//     next tile's global loads are issued before the current tile's MFMAs and written to the other
+//     buffer after.
 //   * Online softmax in fp32 (exp2 with the log2(e) factor folded into the scale); masking is by
 //     selection, and K/V rows past the request's last valid position are never loaded (their
 //     addresses are clamped to the last valid row), so stale or NaN pool slots cannot leak into

@@ -133,7 +133,8 @@ int wavepp_plan_get_items(const wavepp_plan* plan, int32_t* items, int32_t capac
 
 /* Enqueue on `stream` the copy of the plan's metadata into the head of `workspace` (device
  * memory of at least wavepp_plan_workspace_bytes bytes, 256-byte aligned).  The source is a
- * library-owned pinned staging buffer, so the plan may be destroyed right after this returns.
+ * library-owned pinned staging buffer, so the plan may be destroyed right after this returns; the
+ * copy is a small kernel on `stream` that reads that buffer through its device mapping.
  * Kernels enqueued later on the same stream read the metadata from the workspace; a workspace
  * holding another plan's metadata makes them write nothing. */
 int wavepp_attn_plan_upload(const wavepp_plan* plan, void* workspace, size_t ws_bytes, hipStream_t stream);

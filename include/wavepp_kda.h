@@ -88,7 +88,8 @@ size_t wavepp_kda_workspace_bytes(const wavepp_kda_plan_t* plan);
 int wavepp_kda_get_info(const wavepp_kda_plan_t* plan, wavepp_kda_info* info);
 
 /* Enqueue on `stream` the copy of the plan's metadata into `workspace` (device memory of at least
- * wavepp_kda_workspace_bytes, 256-byte aligned) from a library-owned pinned buffer. */
+ * wavepp_kda_workspace_bytes, 256-byte aligned) from a library-owned pinned buffer, by a small copy
+ * kernel on `stream`. */
 int wavepp_kda_upload(const wavepp_kda_plan_t* plan, void* workspace, size_t ws_bytes, hipStream_t stream);
 
 /* Chunked prefill of one KDA layer.  Device pointers with the layouts above; q, k, v, alpha, beta,

@@ -175,10 +175,13 @@ namespace wavepp {
 
 // ---------------------------------------------------------------------------------------------
 // Pinned staging for metadata uploads: a small ring of page-locked buffers per device, each
-// guarded by an event so a buffer is refilled only after its previous copy has completed.
+// guarded by an event so a buffer is refilled only after its previous copy has completed.  The
+// buffers are coherent and mapped into the device's address space; a copy kernel on the caller's
+// stream moves them into the workspace (see launch_upload).
 // ---------------------------------------------------------------------------------------------
 struct StagingSlot {
   void* host = nullptr;
+  void* dev = nullptr;     // the same buffer's device address
   size_t cap = 0;
   hipEvent_t done = nullptr;
   bool pending = false;
@@ -214,17 +217,27 @@ int stage_and_copy(const void* src, size_t bytes, void* dst, hipStream_t stream)
     if (s.host) {
       e = hipHostFree(s.host);
       s.host = nullptr;
+      s.dev = nullptr;
       s.cap = 0;
       if (e != hipSuccess) return set_hip_error(e, "hipHostFree");
     }
     size_t cap = align_up(std::max<size_t>(bytes, 64 << 10), 4096);
-    e = hipHostMalloc(&s.host, cap, hipHostMallocDefault);
+    void* host = nullptr;
+    void* mapped = nullptr;
+    e = hipHostMalloc(&host, cap, hipHostMallocCoherent | hipHostMallocMapped);
     if (e != hipSuccess) return set_hip_error(e, "hipHostMalloc");
+    e = hipHostGetDevicePointer(&mapped, host, 0);
+    if (e != hipSuccess) {
+      (void)hipHostFree(host);
+      return set_hip_error(e, "hipHostGetDevicePointer");
+    }
+    s.host = host;
+    s.dev = mapped;
     s.cap = cap;
   }
   memcpy(s.host, src, bytes);
-  e = hipMemcpyAsync(dst, s.host, bytes, hipMemcpyHostToDevice, stream);
-  if (e != hipSuccess) return set_hip_error(e, "hipMemcpyAsync");
+  e = launch_upload(s.dev, dst, bytes, stream);
+  if (e != hipSuccess) return set_hip_error(e, "metadata upload launch");
   e = hipEventRecord(s.done, stream);
   if (e != hipSuccess) return set_hip_error(e, "hipEventRecord");
   s.pending = true;

@@ -124,5 +124,7 @@ hipError_t launch_append(const DevPlan& p, const void* k_new, const void* v_new,
 hipError_t launch_attention(const DevPlan& p, const void* q, const void* k_pool, const void* v_pool, void* out,
                             float* lse, hipStream_t stream);
 hipError_t launch_merge(const DevPlan& p, void* out, float* lse, hipStream_t stream);
+// Copy `bytes` from device-visible pinned host memory to device memory with a kernel on `stream`.
+hipError_t launch_upload(const void* src, void* dst, size_t bytes, hipStream_t stream);
 
 }  // namespace wavepp

@@ -27,6 +27,8 @@
 
 #include "internal.h"
 
+#include <algorithm>
+
 namespace wavepp {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -627,6 +629,19 @@ __global__ __launch_bounds__(256, 1) void attn_mla_kernel(DevPlan p, const __bf1
 }
 
 // ---------------------------------------------------------------------------------------------
+// Metadata upload: the plan's bytes, read straight from the pinned (coherent, device-mapped)
+// staging buffer and written into the workspace.  A kernel on the launch stream keeps the upload
+// in the compute queue, so the append and attention kernels behind it start without waiting for
+// a DMA engine's completion signal.
+// ---------------------------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void upload_kernel(const u32x4* __restrict__ src, u32x4* __restrict__ dst,
+                                                     int64_t n16, const unsigned char* __restrict__ tail_src,
+                                                     unsigned char* __restrict__ tail_dst, int tail) {
+  for (int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x; i < n16; i += int64_t(gridDim.x) * 256) dst[i] = src[i];
+  if (blockIdx.x == 0 && int(threadIdx.x) < tail) tail_dst[threadIdx.x] = tail_src[threadIdx.x];
+}
+
+// ---------------------------------------------------------------------------------------------
 // Merge of key-range splits: o = sum_s w_s o_s / sum_s w_s with w_s = exp(lse_s - max lse),
 // lse = max + ln sum_s w_s.  Splits are combined in index order, so results are deterministic.
 // ---------------------------------------------------------------------------------------------
@@ -759,6 +774,17 @@ hipError_t launch_attention(const DevPlan& p, const void* q, const void* k_pool,
     return hipErrorInvalidValue;
   }
 #undef WAVEPP_GQA
+  return hipGetLastError();
+}
+
+hipError_t launch_upload(const void* src, void* dst, size_t bytes, hipStream_t stream) {
+  if (bytes == 0) return hipSuccess;
+  const int64_t n16 = int64_t(bytes / 16);
+  const int tail = int(bytes % 16);
+  const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>((n16 + 255) / 256, 1024));
+  hipLaunchKernelGGL(upload_kernel, dim3(unsigned(blocks)), dim3(256), 0, stream, static_cast<const u32x4*>(src),
+                     static_cast<u32x4*>(dst), n16, static_cast<const unsigned char*>(src) + 16 * n16,
+                     static_cast<unsigned char*>(dst) + 16 * n16, tail);
   return hipGetLastError();
 }
 

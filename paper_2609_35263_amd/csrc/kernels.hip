@@ -388,10 +388,14 @@ __global__ __launch_bounds__(256, 1) void attn_mla_kernel(DevPlan p, const __bf1
   constexpr int STR = DQ + 8;           // latent rows in LDS (elements)
   constexpr int CH = DQ / 8;            // 16-byte chunks per latent row
   constexpr int LOADS = KT * CH / 256;  // chunks per thread per tile (18)
-  constexpr int ROUND = LOADS / 3;      // the next tile is staged in three rounds of registers
   constexpr int PPT = (PAGE >= KT) ? 1 : KT / PAGE;
+  // The next tile is staged in NR rounds of registers.  Two rounds, each landing behind an MFMA phase
+  // (logits, then P V); with 16-token pages the page selection needs more registers, and a third,
+  // shorter round behind the softmax keeps that instantiation's spills down.
+  constexpr int NR = PPT == 1 ? 2 : 3;
+  constexpr int ROUND = LOADS / NR;
   constexpr int DW = DV / 4;            // value lanes per wave
-  static_assert(LOADS * 256 == KT * CH && ROUND * 3 == LOADS, "tile covered exactly");
+  static_assert(LOADS * 256 == KT * CH && ROUND * NR == LOADS, "tile covered exactly");
   __shared__ __attribute__((aligned(16))) __bf16 lt[2][KT * STR];
   __shared__ __attribute__((aligned(16))) bf16x8 pl[2][4][64];   // [row block][16-key step][lane]
   __shared__ float xm[2][2][32];                                 // [key block][row block][row]: partial max
@@ -474,7 +478,7 @@ __global__ __launch_bounds__(256, 1) void attn_mla_kernel(DevPlan p, const __bf1
       WAVEPP_MLA_PAGES(t_begin, pg_cur)
       WAVEPP_MLA_PAGES(t_begin + 1, pg_nxt)
 #pragma unroll
-      for (int rd = 0; rd < 3; ++rd) {
+      for (int rd = 0; rd < NR; ++rd) {
         WAVEPP_MLA_LOAD(t_begin, pg_cur, rd * ROUND)
         WAVEPP_MLA_STORE(0, rd * ROUND)
       }
@@ -537,31 +541,40 @@ __global__ __launch_bounds__(256, 1) void attn_mla_kernel(DevPlan p, const __bf1
       l_part += halves_sum(ra + rz);
       pl[rb][2 * kb][lane] = pb[0];
       pl[rb][2 * kb + 1][lane] = pb[1];
-      if (has_next) {
-        WAVEPP_MLA_STORE(buf ^ 1, ROUND)
-        WAVEPP_MLA_LOAD(tile + 1, pg_nxt, 2 * ROUND)
+      if constexpr (NR == 3) {
+        if (has_next) {
+          WAVEPP_MLA_STORE(buf ^ 1, ROUND)
+          WAVEPP_MLA_LOAD(tile + 1, pg_nxt, 2 * ROUND)
+        }
       }
       __syncthreads();
 
       // O^T[d][row] += V^T[d][key] P^T[key][row] on the wave's value lanes, for all 64 rows
       {
         const __bf16* vl = &lt[buf][v_lane];
+        // software-pipelined: the V fragment of step n+1 is read while the MFMA pair of step n runs
+        bf16x4 lo = lds_read_tr(vl);
+        bf16x4 hi = lds_read_tr(vl + 8 * STR);
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks) {
           const bf16x8 p0 = pl[0][ks][lane];
           const bf16x8 p1 = pl[1][ks][lane];
 #pragma unroll
           for (int db = 0; db < DW / 32; ++db) {
-            const bf16x4 lo = lds_read_tr(vl + 16 * ks * STR + 32 * db);
-            const bf16x4 hi = lds_read_tr(vl + (16 * ks + 8) * STR + 32 * db);
             const bf16x8 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+            const int n = ks * (DW / 32) + db + 1;
+            if (n < 4 * (DW / 32)) {
+              const int nks = n / (DW / 32), ndb = n % (DW / 32);
+              lo = lds_read_tr(vl + 16 * nks * STR + 32 * ndb);
+              hi = lds_read_tr(vl + (16 * nks + 8) * STR + 32 * ndb);
+            }
             oacc[0][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, p0, oacc[0][db], 0, 0, 0);
             oacc[1][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, p1, oacc[1][db], 0, 0, 0);
           }
         }
       }
       if (has_next) {
-        WAVEPP_MLA_STORE(buf ^ 1, 2 * ROUND)
+        WAVEPP_MLA_STORE(buf ^ 1, (NR - 1) * ROUND)
         WAVEPP_MLA_PAGES(tile + 2, pg_nxt)
       }
       __syncthreads();

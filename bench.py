@@ -126,9 +126,9 @@ def append_bytes(spec) -> float:
 def cpu_baseline(spec, tensors, budget_s=12.0):
     """Time the fp64 oracle (as it stands) on the host cores on a bounded sample of the same wave.
 
-    Small waves (<= 1 TFLOP) are timed whole; larger ones on random (token, head) rows, each over all
-    of its visible keys, with the sample grown until it takes a few seconds.  The append is done
-    beforehand and is not timed.
+    Small waves (<= 1 TFLOP) are timed whole, repeated until the runs add up to about `budget_s`;
+    larger ones on random (token, head) rows, each over all of its visible keys, with the sample
+    grown until one run takes about `budget_s`.  The append is done beforehand and is not timed.
     """
     import numpy as np
     import oracle
@@ -147,11 +147,15 @@ def cpu_baseline(spec, tensors, budget_s=12.0):
     total_flop = flops_alg(spec)
     if total_flop <= 1e12:
         q = wl.to_bits(tensors["q"])
-        t0 = time.perf_counter()
-        oracle.chunked_prefill(q, k1, v1, spec.prefix_lens, spec.chunk_lens, spec.block_table, **kw)
-        dt = time.perf_counter() - t0
-        flop, n = total_flop, None
-        sample = f"whole {spec.name} wave (all {spec.total_tokens} tokens x {spec.num_q_heads} heads)"
+        runs, dt = 0, 0.0
+        while runs == 0 or (dt < budget_s * 0.8 and runs < 10000):
+            t0 = time.perf_counter()
+            oracle.chunked_prefill(q, k1, v1, spec.prefix_lens, spec.chunk_lens, spec.block_table, **kw)
+            dt += time.perf_counter() - t0
+            runs += 1
+        flop, n = total_flop * runs, None
+        sample = (f"whole {spec.name} wave (all {spec.total_tokens} tokens x {spec.num_q_heads} heads), "
+                  f"{runs} run{'s' if runs > 1 else ''}")
     else:
         rng = np.random.default_rng(0)
         cu = spec.cu_tokens
@@ -168,9 +172,9 @@ def cpu_baseline(spec, tensors, budget_s=12.0):
             oracle.chunked_prefill_rows(qd, k1, v1, spec.prefix_lens, spec.chunk_lens, spec.block_table,
                                         samples, **kw)
             dt = time.perf_counter() - t0
-            if dt >= budget_s / 4 or n >= 1 << 14:
+            if dt >= budget_s * 0.6 or n >= 1 << 16:
                 break
-            n = int(n * min(16.0, max(2.0, budget_s / 2 / max(dt, 1e-3))))
+            n = int(n * min(16.0, max(1.5, budget_s / max(dt, 1e-3))))
         sample = f"{n} random (token, head) rows of the {spec.name} wave, each over all its visible keys"
     return {"value": round(flop / dt / 1e12, 6), "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
             "sample": sample, "seconds": round(dt, 3)}
@@ -366,7 +370,7 @@ def kda_flops_alg(spec) -> float:
 
 def kda_cpu_baseline(spec, tensors, budget_s=12.0):
     """Time the fp64 oracle (as it stands) on the host cores: the first n tokens of the first request,
-    all heads, n grown until the run takes a few seconds.  Reported in new tokens/s of the whole layer."""
+    all heads, n grown until one run takes about `budget_s`.  Reported in new tokens/s of the whole layer."""
     import oracle.kda as okda
     import workloads as wl
     try:
@@ -385,9 +389,9 @@ def kda_cpu_baseline(spec, tensors, budget_s=12.0):
         okda.chunked_prefill(bits["q"], bits["k"], bits["v"], part["alpha"].numpy(), part["beta"].numpy(), pool,
                              [n], [int(spec.state_in[0])], [int(spec.state_out[0])])
         dt = time.perf_counter() - t0
-        if dt >= budget_s / 4 or n >= c0:
+        if dt >= budget_s * 0.6 or n >= c0:
             break
-        n = int(n * min(16.0, max(2.0, budget_s / 2 / max(dt, 1e-3))))
+        n = int(n * min(16.0, max(1.5, budget_s / max(dt, 1e-3))))
     return {"value": round(n / dt, 3), "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
             "sample": f"first {n} tokens of request 0 of the {spec.name} wave, all {spec.num_heads} heads",
             "seconds": round(dt, 3)}

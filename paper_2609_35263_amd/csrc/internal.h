@@ -99,6 +99,11 @@ struct alignas(16) KdaItem {
   int32_t pad[3];
 };
 
+// The metadata upload copies 16-byte words, so every record of a blob is a multiple of 16 bytes.
+static_assert(sizeof(MetaHeader) % 16 == 0 && sizeof(ReqMeta) % 16 == 0 && sizeof(WorkItem) % 16 == 0 &&
+                  sizeof(MergeItem) % 16 == 0 && sizeof(KdaHeader) % 16 == 0 && sizeof(KdaItem) % 16 == 0,
+              "metadata records are whole 16-byte words");
+
 struct KdaDevPlan {
   const KdaHeader* hdr;
   const KdaItem* items;
@@ -124,7 +129,8 @@ hipError_t launch_append(const DevPlan& p, const void* k_new, const void* v_new,
 hipError_t launch_attention(const DevPlan& p, const void* q, const void* k_pool, const void* v_pool, void* out,
                             float* lse, hipStream_t stream);
 hipError_t launch_merge(const DevPlan& p, void* out, float* lse, hipStream_t stream);
-// Copy `bytes` from device-visible pinned host memory to device memory with a kernel on `stream`.
+// Copy `bytes` (a multiple of 16, both pointers 16-byte aligned) from device-visible pinned host
+// memory to device memory with a kernel on `stream`.
 hipError_t launch_upload(const void* src, void* dst, size_t bytes, hipStream_t stream);
 
 }  // namespace wavepp

@@ -648,10 +648,8 @@ __global__ __launch_bounds__(256, 1) void attn_mla_kernel(DevPlan p, const __bf1
 // a DMA engine's completion signal.
 // ---------------------------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void upload_kernel(const u32x4* __restrict__ src, u32x4* __restrict__ dst,
-                                                     int64_t n16, const unsigned char* __restrict__ tail_src,
-                                                     unsigned char* __restrict__ tail_dst, int tail) {
+                                                     int64_t n16) {
   for (int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x; i < n16; i += int64_t(gridDim.x) * 256) dst[i] = src[i];
-  if (blockIdx.x == 0 && int(threadIdx.x) < tail) tail_dst[threadIdx.x] = tail_src[threadIdx.x];
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -670,49 +668,71 @@ __global__ __launch_bounds__(256) void merge_kernel(DevPlan p, __bf16* __restric
   if (lrow >= mi.rows) return;
   const ReqMeta rm = p.reqs[mi.req];
   const int Hq = p.num_q_heads, G = Hq / p.num_kv_heads;
-  // Partials are read four splits at a time, so that their loads are in flight together; the
-  // accumulation order stays s = 0, 1, ..., nsplit - 1 (deterministic).  A split that saw no key has
-  // lse = -inf and an all-zero partial row, which gets weight 0.
+  // The accumulation order is s = 0, 1, ..., nsplit - 1 (deterministic).  A split that saw no key
+  // has lse = -inf and an all-zero partial row, which gets weight 0.  Up to SB splits, every LSE and
+  // partial is loaded at once (one memory round trip); beyond that, two passes read four splits at
+  // a time.  Both paths do the same arithmetic in the same order.
+  constexpr int SB = 16;
   const int ns = mi.nsplit;
   const float* __restrict__ lp = p.lpart + mi.part + lrow;
   const float* __restrict__ op = p.opart + (int64_t(mi.part) + lrow) * DV + 4 * c4;
   const int64_t ostep = int64_t(mi.rows) * DV;
   float mx = -INFINITY;
-  {
-    int s = 0;
-    for (; s + 4 <= ns; s += 4) {
-      float l[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) l[u] = lp[(s + u) * mi.rows];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) mx = fmaxf(mx, l[u]);
-    }
-    for (; s < ns; ++s) mx = fmaxf(mx, lp[s * mi.rows]);
-  }
   f32x4 acc = f32x4{};
   float wsum = 0.0f;
-  {
-    int s = 0;
-    for (; s + 4 <= ns; s += 4) {
-      float l[4];
-      f32x4 v[4];
+  if (ns <= SB) {
+    float l[SB];
+    f32x4 v[SB];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        l[u] = lp[(s + u) * mi.rows];
-        v[u] = *reinterpret_cast<const f32x4*>(op + (s + u) * ostep);
-      }
+    for (int u = 0; u < SB; ++u) {
+      l[u] = u < ns ? lp[u * mi.rows] : -INFINITY;
+      v[u] = u < ns ? *reinterpret_cast<const f32x4*>(op + u * ostep) : f32x4{};
+    }
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < SB; ++u) mx = fmaxf(mx, l[u]);
+#pragma unroll
+    for (int u = 0; u < SB; ++u) {
+      if (u < ns) {
         const float w = (l[u] == -INFINITY) ? 0.0f : fast_exp2((l[u] - mx) * kLog2e);
         acc += w * v[u];
         wsum += w;
       }
     }
-    for (; s < ns; ++s) {
-      const float l = lp[s * mi.rows];
-      const float w = (l == -INFINITY) ? 0.0f : fast_exp2((l - mx) * kLog2e);
-      acc += w * *reinterpret_cast<const f32x4*>(op + s * ostep);
-      wsum += w;
+  } else {
+    {
+      int s = 0;
+      for (; s + 4 <= ns; s += 4) {
+        float l[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) l[u] = lp[(s + u) * mi.rows];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) mx = fmaxf(mx, l[u]);
+      }
+      for (; s < ns; ++s) mx = fmaxf(mx, lp[s * mi.rows]);
+    }
+    {
+      int s = 0;
+      for (; s + 4 <= ns; s += 4) {
+        float l[4];
+        f32x4 v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          l[u] = lp[(s + u) * mi.rows];
+          v[u] = *reinterpret_cast<const f32x4*>(op + (s + u) * ostep);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const float w = (l[u] == -INFINITY) ? 0.0f : fast_exp2((l[u] - mx) * kLog2e);
+          acc += w * v[u];
+          wsum += w;
+        }
+      }
+      for (; s < ns; ++s) {
+        const float l = lp[s * mi.rows];
+        const float w = (l == -INFINITY) ? 0.0f : fast_exp2((l - mx) * kLog2e);
+        acc += w * *reinterpret_cast<const f32x4*>(op + s * ostep);
+        wsum += w;
+      }
     }
   }
   const float inv = 1.0f / wsum;
@@ -792,12 +812,13 @@ hipError_t launch_attention(const DevPlan& p, const void* q, const void* k_pool,
 
 hipError_t launch_upload(const void* src, void* dst, size_t bytes, hipStream_t stream) {
   if (bytes == 0) return hipSuccess;
+  // metadata blobs are built from 16-byte-aligned records
+  if (bytes % 16 || reinterpret_cast<uintptr_t>(src) % 16 || reinterpret_cast<uintptr_t>(dst) % 16)
+    return hipErrorInvalidValue;
   const int64_t n16 = int64_t(bytes / 16);
-  const int tail = int(bytes % 16);
-  const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>((n16 + 255) / 256, 1024));
+  const int64_t blocks = std::min<int64_t>((n16 + 255) / 256, 1024);
   hipLaunchKernelGGL(upload_kernel, dim3(unsigned(blocks)), dim3(256), 0, stream, static_cast<const u32x4*>(src),
-                     static_cast<u32x4*>(dst), n16, static_cast<const unsigned char*>(src) + 16 * n16,
-                     static_cast<unsigned char*>(dst) + 16 * n16, tail);
+                     static_cast<u32x4*>(dst), n16);
   return hipGetLastError();
 }
 

@@ -70,8 +70,10 @@ def test_custom_shapes(case):
     check_wave(spec, seed=len(prefix) * 13 + B)
 
 
-@pytest.mark.parametrize("splits", [1, 2, 7])
+@pytest.mark.parametrize("splits", [1, 2, 7, 24])
 def test_split_invariance_and_determinism(splits):
+    """24 splits gives the longest items one split per 128-key tile (24 of them), past the merge
+    kernel's single-round-trip limit of 16, and the shorter ones 16 or fewer."""
     torch = _torch()
     spec = wl.custom_wave(32, 8, 128, 128, 64, [1000, 64, 3000], [300, 129, 64], seed=9, name="split")
     g, ref, t = check_wave(spec, seed=99, max_splits=splits)

@@ -352,16 +352,34 @@ __global__ __launch_bounds__(256, 1) void kda_prefill_kernel(KdaDevPlan p, const
     const int tb1 = wave == 0 ? 0 : 1, sb1 = wave == 2 ? 1 : 0;
     f32x16 accA = {}, accP = {};
     if (wave < 3) {
+      // the operands of step kc + 1 are read while step kc's two products run
+      const __bf16* kp = &ls.kt[(32 * tb1 + col) * QS + 8 * hf];
+      const __bf16* qp = &ls.qt[(32 * tb1 + col) * QS + 8 * hf];
+      const __bf16* rp = &ls.kr[(32 * sb1 + col) * RS + 8 * hf];
+      auto ld4 = [](const __bf16* p) { return cat(*reinterpret_cast<const bf16x4*>(p), *reinterpret_cast<const bf16x4*>(p + 4)); };
+      bf16x8 ak = ld4(kp), aq = ld4(qp), b = *reinterpret_cast<const bf16x8*>(rp);
 #pragma unroll
       for (int kc = 0; kc < kD / 16; ++kc) {
-        const __bf16* kp = &ls.kt[(32 * tb1 + col) * QS + 16 * kc + 8 * hf];
-        const __bf16* qp = &ls.qt[(32 * tb1 + col) * QS + 16 * kc + 8 * hf];
-        const bf16x8 ak = cat(*reinterpret_cast<const bf16x4*>(kp), *reinterpret_cast<const bf16x4*>(kp + 4));
-        const bf16x8 aq = cat(*reinterpret_cast<const bf16x4*>(qp), *reinterpret_cast<const bf16x4*>(qp + 4));
-        const bf16x8 b = *reinterpret_cast<const bf16x8*>(&ls.kr[(32 * sb1 + col) * RS + 16 * kc + 8 * hf]);
+        bf16x8 nk = ak, nq = aq, nb = b;
+        if (kc + 1 < kD / 16) {
+          nk = ld4(kp + 16 * (kc + 1));
+          nq = ld4(qp + 16 * (kc + 1));
+          nb = *reinterpret_cast<const bf16x8*>(rp + 16 * (kc + 1));
+        }
         accA = mfma(ak, b, accA);
         accP = mfma(aq, b, accP);
+        ak = nk;
+        aq = nq;
+        b = nb;
       }
+      // keep the scheduler from sinking the reads back next to their products
+      __builtin_amdgcn_sched_group_barrier(0x100, 5, 0);
+#pragma unroll
+      for (int i = 0; i < kD / 16 - 1; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x100, 5, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
     }
     // slow channels: exact pairwise terms in log2 space, 16 channels per batch, re-read from memory
     for (int base = 0; base < nslow; base += kSlowBatch) {
@@ -532,16 +550,26 @@ __global__ __launch_bounds__(256, 1) void kda_prefill_kernel(KdaDevPlan p, const
         sB[ib][1] = acc_to_b(S[ib], 1);
       }
       f32x16 accE[2] = {}, accO[2] = {};
+      {
+        // software-pipelined: the A operands of step n + 1 are read while step n's MFMAs run
+        bf16x8 ak = lds_a_perm(&ls.kt[col * QS], 4 * hf);
+        bf16x8 aq = lds_a_perm(&ls.qt[col * QS], 4 * hf);
 #pragma unroll
-      for (int ib = 0; ib < 4; ++ib)
-#pragma unroll
-        for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-          for (int tb = 0; tb < 2; ++tb) {
-            const int cb = 32 * ib + 16 * kk + 4 * hf;
-            accE[tb] = mfma(lds_a_perm(&ls.kt[(32 * tb + col) * QS], cb), sB[ib][kk], accE[tb]);
-            accO[tb] = mfma(lds_a_perm(&ls.qt[(32 * tb + col) * QS], cb), sB[ib][kk], accO[tb]);
+        for (int n = 0; n < 16; ++n) {
+          const int ib = n >> 2, kk = (n >> 1) & 1, tb = n & 1;
+          bf16x8 nk = ak, nq = aq;
+          if (n + 1 < 16) {
+            const int m = n + 1;
+            const int cb = 32 * (m >> 2) + 16 * ((m >> 1) & 1) + 4 * hf;
+            nk = lds_a_perm(&ls.kt[(32 * (m & 1) + col) * QS], cb);
+            nq = lds_a_perm(&ls.qt[(32 * (m & 1) + col) * QS], cb);
           }
+          accE[tb] = mfma(ak, sB[ib][kk], accE[tb]);
+          accO[tb] = mfma(aq, sB[ib][kk], accO[tb]);
+          ak = nk;
+          aq = nq;
+        }
+      }
       // R = beta (V - E), in place in accE.  V[t0 + r][j] for r = 0..3 comes from the transposing
       // read: lane 4m + g of each 16-lane group addresses row t0 + m at column 4g of its group.
       const int j = j0 + col;
@@ -565,15 +593,23 @@ __global__ __launch_bounds__(256, 1) void kda_prefill_kernel(KdaDevPlan p, const
         rB[tb][0] = acc_to_b(accE[tb], 0);
         rB[tb][1] = acc_to_b(accE[tb], 1);
       }
-      // U = T R (T lower-triangular: block row tb uses block columns sb <= tb)
+      // U = T R (T lower-triangular: block row tb uses block columns sb <= tb).  The six products
+      // run in the order (tb, sb, kk) = (0,0,0) (0,0,1) (1,0,0) (1,0,1) (1,1,0) (1,1,1); each A
+      // operand is read while the previous product runs.  O += P U below uses the same order.
       f32x16 accU[2] = {};
+      {
+        bf16x8 a = lds_a_perm(&ls.tm[col * CS], 4 * hf);
 #pragma unroll
-      for (int tb = 0; tb < 2; ++tb) {
-        const __bf16* tr = &ls.tm[(32 * tb + col) * CS];
-#pragma unroll
-        for (int sb = 0; sb <= tb; ++sb)
-#pragma unroll
-          for (int kk = 0; kk < 2; ++kk) accU[tb] = mfma(lds_a_perm(tr, 32 * sb + 16 * kk + 4 * hf), rB[sb][kk], accU[tb]);
+        for (int n = 0; n < 6; ++n) {
+          const int tb = n < 2 ? 0 : 1, sb = n < 4 ? 0 : 1, kk = n & 1;
+          bf16x8 na = a;
+          if (n + 1 < 6) {
+            const int m = n + 1;
+            na = lds_a_perm(&ls.tm[(32 * (m < 2 ? 0 : 1) + col) * CS], 32 * (m < 4 ? 0 : 1) + 16 * (m & 1) + 4 * hf);
+          }
+          accU[tb] = mfma(a, rB[sb][kk], accU[tb]);
+          a = na;
+        }
       }
       bf16x8 uB[2][2];
 #pragma unroll
@@ -582,35 +618,53 @@ __global__ __launch_bounds__(256, 1) void kda_prefill_kernel(KdaDevPlan p, const
         uB[tb][1] = acc_to_b(accU[tb], 1);
       }
       // O += P U, then store the valid rows
+      {
+        bf16x8 a = lds_a_perm(&ls.pm[col * CS], 4 * hf);
+#pragma unroll
+        for (int n = 0; n < 6; ++n) {
+          const int tb = n < 2 ? 0 : 1, sb = n < 4 ? 0 : 1, kk = n & 1;
+          bf16x8 na = a;
+          if (n + 1 < 6) {
+            const int m = n + 1;
+            na = lds_a_perm(&ls.pm[(32 * (m < 2 ? 0 : 1) + col) * CS], 32 * (m < 4 ? 0 : 1) + 16 * (m & 1) + 4 * hf);
+          }
+          accO[tb] = mfma(a, uB[sb][kk], accO[tb]);
+          a = na;
+        }
+      }
 #pragma unroll
       for (int tb = 0; tb < 2; ++tb) {
-        const __bf16* pr = &ls.pm[(32 * tb + col) * CS];
-#pragma unroll
-        for (int sb = 0; sb <= tb; ++sb)
-#pragma unroll
-          for (int kk = 0; kk < 2; ++kk) accO[tb] = mfma(lds_a_perm(pr, 32 * sb + 16 * kk + 4 * hf), uB[sb][kk], accO[tb]);
 #pragma unroll
         for (int reg = 0; reg < 16; ++reg) {
           const int t = 32 * tb + 8 * (reg >> 2) + 4 * hf + (reg & 3);
           ls.ob[t * RS + j] = static_cast<__bf16>(accO[tb][reg]);
         }
       }
-      // S = Diag(gamma_C) S + Kbar^T U
+      // S = Diag(gamma_C) S + Kbar^T U: 16 products in the order (ib, sb, kk), each A operand read
+      // while the previous product runs
+      {
+        bf16x8 a = lds_a_perm(&ls.kbt[col * CS], 4 * hf);
 #pragma unroll
-      for (int ib = 0; ib < 4; ++ib) {
+        for (int n = 0; n < 16; ++n) {
+          const int ib = n >> 2, sb = (n >> 1) & 1, kk = n & 1;
+          if ((n & 3) == 0) {
 #pragma unroll
-        for (int b = 0; b < 4; ++b) {
-          const float4 gcv = *reinterpret_cast<const float4*>(&ls.gc[32 * ib + 8 * b + 4 * hf]);
-          S[ib][4 * b + 0] *= gcv.x;
-          S[ib][4 * b + 1] *= gcv.y;
-          S[ib][4 * b + 2] *= gcv.z;
-          S[ib][4 * b + 3] *= gcv.w;
+            for (int b = 0; b < 4; ++b) {
+              const float4 gcv = *reinterpret_cast<const float4*>(&ls.gc[32 * ib + 8 * b + 4 * hf]);
+              S[ib][4 * b + 0] *= gcv.x;
+              S[ib][4 * b + 1] *= gcv.y;
+              S[ib][4 * b + 2] *= gcv.z;
+              S[ib][4 * b + 3] *= gcv.w;
+            }
+          }
+          bf16x8 na = a;
+          if (n + 1 < 16) {
+            const int m = n + 1;
+            na = lds_a_perm(&ls.kbt[(32 * (m >> 2) + col) * CS], 32 * ((m >> 1) & 1) + 16 * (m & 1) + 4 * hf);
+          }
+          S[ib] = mfma(a, uB[sb][kk], S[ib]);
+          a = na;
         }
-        const __bf16* kr = &ls.kbt[(32 * ib + col) * CS];
-#pragma unroll
-        for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-          for (int kk = 0; kk < 2; ++kk) S[ib] = mfma(lds_a_perm(kr, 32 * sb + 16 * kk + 4 * hf), uB[sb][kk], S[ib]);
       }
     }
     lds_barrier();

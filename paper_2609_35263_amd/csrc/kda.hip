@@ -458,12 +458,25 @@ __global__ __launch_bounds__(256, 1) void kda_prefill_kernel(KdaDevPlan p, const
       // diagonal 16 x 16 blocks by forward substitution: wave -> block, lane -> column
       const int a0 = 16 * wave, jc = lane & 15;
       float xs[16];
+      // row t + 1 of the block is read while row t is solved
+      float4 rc[4] = {}, rn[4] = {};
 #pragma unroll
       for (int t = 0; t < 16; ++t) {
+        if (t + 1 < 16) {
+#pragma unroll
+          for (int k = 0; k < 4; ++k)
+            if (4 * k < t + 1) rn[k] = *reinterpret_cast<const float4*>(&ls.a[(a0 + t + 1) * AS + a0 + 4 * k]);
+        }
         float acc = (t == jc) ? 1.0f : 0.0f;
 #pragma unroll
-        for (int u = 0; u < t; ++u) acc -= ls.a[(a0 + t) * AS + a0 + u] * xs[u];
+        for (int u = 0; u < t; ++u) {
+          const float4 r = rc[u >> 2];
+          const float c = (u & 3) == 0 ? r.x : (u & 3) == 1 ? r.y : (u & 3) == 2 ? r.z : r.w;
+          acc -= c * xs[u];
+        }
         xs[t] = acc;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) rc[k] = rn[k];
       }
       if (lane < 16) {
 #pragma unroll
@@ -481,22 +494,50 @@ __global__ __launch_bounds__(256, 1) void kda_prefill_kernel(KdaDevPlan p, const
       const int which = tid >> 7, e = tid & 127, tr = e >> 3, jc = 2 * (e & 7);
       const int ba = 2 * which + 1, bb = 2 * which;
       float x0 = 0.0f, x1 = 0.0f;
+      {
+        // all sixteen (A, D) pairs are read before the sums start
+        float av[16];
+        float2 d[16];
 #pragma unroll
-      for (int u = 0; u < 16; ++u) {
-        const float av = ls.a[(16 * ba + tr) * AS + 16 * bb + u];
-        const float2 d = *reinterpret_cast<const float2*>(&ls.tf[(16 * bb + u) * AS + 16 * bb + jc]);
-        x0 += av * d.x;
-        x1 += av * d.y;
+        for (int k = 0; k < 4; ++k) {
+          const float4 a4 = *reinterpret_cast<const float4*>(&ls.a[(16 * ba + tr) * AS + 16 * bb + 4 * k]);
+          av[4 * k] = a4.x;
+          av[4 * k + 1] = a4.y;
+          av[4 * k + 2] = a4.z;
+          av[4 * k + 3] = a4.w;
+        }
+#pragma unroll
+        for (int u = 0; u < 16; ++u) d[u] = *reinterpret_cast<const float2*>(&ls.tf[(16 * bb + u) * AS + 16 * bb + jc]);
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {
+          x0 += av[u] * d[u].x;
+          x1 += av[u] * d[u].y;
+        }
       }
       ls.x[which][tr * 17 + jc] = x0;
       ls.x[which][tr * 17 + jc + 1] = x1;
       lds_barrier();
       float y0 = 0.0f, y1 = 0.0f;
+      {
+        float dv[16], xa[16], xb[16];
 #pragma unroll
-      for (int u = 0; u < 16; ++u) {
-        const float dv = ls.tf[(16 * ba + tr) * AS + 16 * ba + u];
-        y0 -= dv * ls.x[which][u * 17 + jc];
-        y1 -= dv * ls.x[which][u * 17 + jc + 1];
+        for (int k = 0; k < 4; ++k) {
+          const float4 d4 = *reinterpret_cast<const float4*>(&ls.tf[(16 * ba + tr) * AS + 16 * ba + 4 * k]);
+          dv[4 * k] = d4.x;
+          dv[4 * k + 1] = d4.y;
+          dv[4 * k + 2] = d4.z;
+          dv[4 * k + 3] = d4.w;
+        }
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {
+          xa[u] = ls.x[which][u * 17 + jc];
+          xb[u] = ls.x[which][u * 17 + jc + 1];
+        }
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {
+          y0 -= dv[u] * xa[u];
+          y1 -= dv[u] * xb[u];
+        }
       }
       ls.tf[(16 * ba + tr) * AS + 16 * bb + jc] = y0;
       ls.tf[(16 * ba + tr) * AS + 16 * bb + jc + 1] = y1;
@@ -576,17 +617,24 @@ __global__ __launch_bounds__(256, 1) void kda_prefill_kernel(KdaDevPlan p, const
       const int grp = lane >> 4, li = lane & 15;
       const int jg = j0 + 16 * (grp & 1) + 4 * (li & 3);
 #pragma unroll
-      for (int tb = 0; tb < 2; ++tb)
+      for (int tb = 0; tb < 2; ++tb) {
+        // the four V fragments and betas of a block row are read before any is used
+        bf16x4 vv[4];
+        float4 bt[4];
 #pragma unroll
         for (int b = 0; b < 4; ++b) {
           const int t0 = 32 * tb + 8 * b + 4 * hf;
-          const bf16x4 vv = lds_read_tr(&ls.v[(t0 + (li >> 2)) * VS + jg]);
-          const float4 bt = *reinterpret_cast<const float4*>(&ls.beta[t0]);
-          const float bs[4] = {bt.x, bt.y, bt.z, bt.w};
+          vv[b] = lds_read_tr(&ls.v[(t0 + (li >> 2)) * VS + jg]);
+          bt[b] = *reinterpret_cast<const float4*>(&ls.beta[t0]);
+        }
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+          const float bs[4] = {bt[b].x, bt[b].y, bt[b].z, bt[b].w};
 #pragma unroll
           for (int r = 0; r < 4; ++r)
-            accE[tb][4 * b + r] = bs[r] * (static_cast<float>(vv[r]) - accE[tb][4 * b + r]);
+            accE[tb][4 * b + r] = bs[r] * (static_cast<float>(vv[b][r]) - accE[tb][4 * b + r]);
         }
+      }
       bf16x8 rB[2][2];
 #pragma unroll
       for (int tb = 0; tb < 2; ++tb) {
@@ -644,17 +692,26 @@ __global__ __launch_bounds__(256, 1) void kda_prefill_kernel(KdaDevPlan p, const
       // while the previous product runs
       {
         bf16x8 a = lds_a_perm(&ls.kbt[col * CS], 4 * hf);
+        // the decays of block row ib + 1 are read while block row ib is updated
+        float4 gcur[4], gnxt[4];
+#pragma unroll
+        for (int b = 0; b < 4; ++b) gcur[b] = *reinterpret_cast<const float4*>(&ls.gc[8 * b + 4 * hf]);
 #pragma unroll
         for (int n = 0; n < 16; ++n) {
           const int ib = n >> 2, sb = (n >> 1) & 1, kk = n & 1;
           if ((n & 3) == 0) {
+            if (ib + 1 < 4) {
+#pragma unroll
+              for (int b = 0; b < 4; ++b)
+                gnxt[b] = *reinterpret_cast<const float4*>(&ls.gc[32 * (ib + 1) + 8 * b + 4 * hf]);
+            }
 #pragma unroll
             for (int b = 0; b < 4; ++b) {
-              const float4 gcv = *reinterpret_cast<const float4*>(&ls.gc[32 * ib + 8 * b + 4 * hf]);
-              S[ib][4 * b + 0] *= gcv.x;
-              S[ib][4 * b + 1] *= gcv.y;
-              S[ib][4 * b + 2] *= gcv.z;
-              S[ib][4 * b + 3] *= gcv.w;
+              S[ib][4 * b + 0] *= gcur[b].x;
+              S[ib][4 * b + 1] *= gcur[b].y;
+              S[ib][4 * b + 2] *= gcur[b].z;
+              S[ib][4 * b + 3] *= gcur[b].w;
+              gcur[b] = gnxt[b];
             }
           }
           bf16x8 na = a;

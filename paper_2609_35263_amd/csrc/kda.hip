@@ -437,11 +437,13 @@ __global__ __launch_bounds__(256, 1) void kda_prefill_kernel(KdaDevPlan p, const
     if (nslow > 0) lds_barrier();   // the batch scratch shares storage with A
     if (wave < 3) {
       const int s = 32 * sb1 + col;
+      float4 btv[4];
+#pragma unroll
+      for (int b = 0; b < 4; ++b) btv[b] = *reinterpret_cast<const float4*>(&ls.beta[32 * tb1 + 8 * b + 4 * hf]);
 #pragma unroll
       for (int b = 0; b < 4; ++b) {
         const int t0 = 32 * tb1 + 8 * b + 4 * hf;
-        const float4 bt = *reinterpret_cast<const float4*>(&ls.beta[t0]);
-        const float bs[4] = {bt.x, bt.y, bt.z, bt.w};
+        const float bs[4] = {btv[b].x, btv[b].y, btv[b].z, btv[b].w};
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int t = t0 + r;

@@ -50,8 +50,19 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 
 // ---------------------------------------------------------------------------------------------
 // Append: token t of request r -> page bt[r][(p_r + i) / B], slot (p_r + i) % B, all KV heads.
-// One thread moves one 16-byte chunk; the flat index runs over (token, kv head, chunk).
+// One workgroup moves kAppendTokens consecutive packed tokens; for each token its threads move the
+// Hkv * (DK + DV) / 8 16-byte chunks (the workgroup has that many threads rounded up to a whole
+// wave, at most 256).  The token's request and page are uniform across the
+// workgroup, so they are looked up once, with scalar loads through the constant address space
+// (the kernel never writes the metadata).
 // ---------------------------------------------------------------------------------------------
+constexpr int kAppendTokens = 8;
+
+template <typename T>
+__device__ __forceinline__ T const_load(const T* ptr) {
+  return *((const __attribute__((address_space(4))) T*)(ptr));
+}
+
 template <int DK, int DV>
 __global__ __launch_bounds__(256) void append_kernel(DevPlan p, const uint4* __restrict__ k_new,
                                                      const uint4* __restrict__ v_new, uint4* __restrict__ k_pool,
@@ -59,29 +70,35 @@ __global__ __launch_bounds__(256) void append_kernel(DevPlan p, const uint4* __r
   if (!meta_ok(p)) return;
   constexpr int KC = DK / 8, VC = DV / 8, UC = KC + VC;
   const int Hkv = p.num_kv_heads;
-  const int64_t units = p.total_tokens * Hkv * UC;
+  const int per_tok = Hkv * UC;
   const int B = p.page_size;
-  for (int64_t u = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; u < units; u += int64_t(gridDim.x) * blockDim.x) {
-    const int64_t per_tok = int64_t(Hkv) * UC;
-    const int t = int(u / per_tok);
-    const int rem = int(u - int64_t(t) * per_tok);
-    const int h = rem / UC;
-    const int c = rem - h * UC;
-    // request holding token t: the last r with cu_r <= t (idle lanes share cu with the next one)
-    int lo = 0, hi = p.num_requests - 1;
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (p.reqs[mid].cu <= t) lo = mid; else hi = mid - 1;
-    }
-    const ReqMeta rm = p.reqs[lo];
-    const int pos = rm.prefix + (t - rm.cu);
-    const int64_t page = p.bt[rm.bt_row + pos / B];
+  const int64_t T = p.total_tokens;
+  const int64_t t0 = int64_t(blockIdx.x) * kAppendTokens;
+  // request holding token t0: the last r with cu_r <= t0 (requests with no chunk share cu with the next)
+  int lo = 0, hi = p.num_requests - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (const_load(&p.reqs[mid].cu) <= t0) lo = mid; else hi = mid - 1;
+  }
+  int r = lo;
+#pragma unroll
+  for (int i = 0; i < kAppendTokens; ++i) {
+    const int64_t t = t0 + i;
+    if (t >= T) break;
+    while (r + 1 < p.num_requests && const_load(&p.reqs[r + 1].cu) <= t) ++r;
+    const ReqMeta* rq = &p.reqs[r];
+    const int pos = const_load(&rq->prefix) + int(t - const_load(&rq->cu));
+    const int64_t page = const_load(&p.bt[const_load(&rq->bt_row) + pos / B]);
     const int slot = pos % B;
-    if (c < KC) {
-      k_pool[((page * Hkv + h) * B + slot) * KC + c] = k_new[(int64_t(t) * Hkv + h) * KC + c];
-    } else {
-      const int cv = c - KC;
-      v_pool[((page * Hkv + h) * B + slot) * VC + cv] = v_new[(int64_t(t) * Hkv + h) * VC + cv];
+    for (int u = threadIdx.x; u < per_tok; u += blockDim.x) {
+      const int h = u / UC;
+      const int c = u - h * UC;
+      if (c < KC) {
+        k_pool[((page * Hkv + h) * B + slot) * KC + c] = k_new[(t * Hkv + h) * KC + c];
+      } else {
+        const int cv = c - KC;
+        v_pool[((page * Hkv + h) * B + slot) * VC + cv] = v_new[(t * Hkv + h) * VC + cv];
+      }
     }
   }
 }
@@ -753,19 +770,21 @@ __global__ __launch_bounds__(256) void merge_kernel(DevPlan p, __bf16* __restric
 hipError_t launch_append(const DevPlan& p, const void* k_new, const void* v_new, void* k_pool, void* v_pool,
                          hipStream_t stream) {
   const int dk = p.head_dim_qk, dv = p.kv_shared ? 0 : p.head_dim_v;
-  const int64_t units = p.total_tokens * p.num_kv_heads * ((dk + dv) / 8);
-  if (units == 0) return hipSuccess;
-  const int64_t blocks = std::min<int64_t>((units + 255) / 256, 65536);
+  if (p.total_tokens == 0) return hipSuccess;
+  const int64_t blocks = (p.total_tokens + kAppendTokens - 1) / kAppendTokens;
+  if (blocks > INT32_MAX) return hipErrorInvalidValue;
+  const int per_tok = p.num_kv_heads * ((dk + dv) / 8);
+  const int threads = std::min(256, (per_tok + 63) / 64 * 64);
   auto kn = static_cast<const uint4*>(k_new);
   auto vn = static_cast<const uint4*>(v_new);
   auto kp = static_cast<uint4*>(k_pool);
   auto vp = static_cast<uint4*>(v_pool);
   if (dk == 64 && dv == 64)
-    hipLaunchKernelGGL((append_kernel<64, 64>), dim3(blocks), dim3(256), 0, stream, p, kn, vn, kp, vp);
+    hipLaunchKernelGGL((append_kernel<64, 64>), dim3(blocks), dim3(threads), 0, stream, p, kn, vn, kp, vp);
   else if (dk == 128 && dv == 128)
-    hipLaunchKernelGGL((append_kernel<128, 128>), dim3(blocks), dim3(256), 0, stream, p, kn, vn, kp, vp);
+    hipLaunchKernelGGL((append_kernel<128, 128>), dim3(blocks), dim3(threads), 0, stream, p, kn, vn, kp, vp);
   else if (dk == 576 && dv == 0)
-    hipLaunchKernelGGL((append_kernel<576, 0>), dim3(blocks), dim3(256), 0, stream, p, kn, vn, kp, vp);
+    hipLaunchKernelGGL((append_kernel<576, 0>), dim3(blocks), dim3(threads), 0, stream, p, kn, vn, kp, vp);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

@@ -4,7 +4,13 @@ A step is one pass of the whole hot path over one wave: host plan -> metadata up
 attention (-> split merge), once per layer of the workload.  Inputs are resident in HBM before the
 timed region.  Prints ONE JSON line.
 
-    python bench.py [--steps K] [--warmup W] [--config 2|1|3|4|5|6p|small16...] [--no-cpu-baseline]
+    python bench.py [--steps K] [--warmup W] [--config 5|1|2|3|4|6p|small16...] [--extras 3,4|none]
+                    [--no-cpu-baseline]
+
+The default headline is the latent-attention wave (8 requests, 131072 cached + 8192 new tokens each,
+128 heads over a 576-wide latent), the largest wave that fits one GPU; the grouped-query waves named
+by --extras (default: the shared-prefix wave and the four-layer concurrency-128 wave) are measured
+after it and reported under "extra".
 
 Metric: attention TFLOP/s (algorithmic FLOP = 2 * Hq * (d_qk + d_v) * sum_r [c_r p_r + c_r (c_r + 1) / 2]
 per layer, exact causal pairs only), new tokens/s, % of the bf16 dense MFMA peak.
@@ -133,11 +139,8 @@ def cpu_baseline(spec, tensors, budget_s=12.0):
     import numpy as np
     import oracle
     import workloads as wl
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:
-        threads = os.cpu_count() or 1
+    host = host_cpu_info()
+    threads = host["blas_threads"] or host["cpu_count"]
     pools = {k: wl.to_bits(tensors[k]) for k in ("k_pool", "v_pool", "k_new", "v_new")}
     k1, v1 = oracle.append_kv(pools["k_pool"], pools["v_pool"], pools["k_new"], pools["v_new"], spec.prefix_lens,
                               spec.chunk_lens, spec.block_table, spec.page_size)
@@ -177,7 +180,31 @@ def cpu_baseline(spec, tensors, budget_s=12.0):
             n = int(n * min(16.0, max(1.5, budget_s / max(dt, 1e-3))))
         sample = f"{n} random (token, head) rows of the {spec.name} wave, each over all its visible keys"
     return {"value": round(flop / dt / 1e12, 6), "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
-            "sample": sample, "seconds": round(dt, 3)}
+            "sample": sample, "seconds": round(dt, 3), **host}
+
+
+def host_cpu_info() -> dict:
+    """The host the oracle runs on: logical CPUs, CPU model (lscpu) and the BLAS library's thread
+    count (the numpy fp64 oracle's matrix products run on that pool)."""
+    info = {"cpu_count": os.cpu_count(), "cpu_model": None, "blas_threads": None, "blas": None}
+    try:
+        import subprocess
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in out.splitlines():
+            if line.lower().startswith("model name"):
+                info["cpu_model"] = line.split(":", 1)[1].strip()
+                break
+    except Exception:
+        pass
+    try:
+        from threadpoolctl import threadpool_info
+        blas = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        if blas:
+            info["blas_threads"] = int(max(i.get("num_threads", 1) for i in blas))
+            info["blas"] = f"{blas[0].get('internal_api')} {blas[0].get('version')}"
+    except Exception:
+        pass
+    return info
 
 
 def main():
@@ -186,7 +213,11 @@ def main():
     ap.add_argument("--steps", type=int, default=None, help="timed steps (default: about one second of work)")
     ap.add_argument("--warmup", type=int, default=None,
                     help="untimed steps first (default: max(0.3 s, min(2 s, 300 steps)))")
-    ap.add_argument("--config", default="2")
+    ap.add_argument("--config", default="5",
+                    help="the headline wave (default 5: the latent-attention wave, the largest that fits one GPU)")
+    ap.add_argument("--extras", default="3,4",
+                    help="comma-separated waves also measured after the headline and reported under 'extra' "
+                         "(each with the default warm-up and about one second of timed steps); 'none' for none")
     ap.add_argument("--max-splits", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -210,28 +241,67 @@ def main():
     if str(args.config) == "peak":
         return main_peak(args)
 
+    import torch
+    import paper_2609_35263_amd as wp
+
+    wp.load_library()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    res = measure_wave(str(args.config), dev, args.warmup, args.steps, args.max_splits,
+                       calib_mib=args.copy_calibration_mib)
+    # what the matrix cores sustain on this chip with random-bit operands (a power-limited clock), as
+    # context for the nominal peak; run after the timed region
+    p_tf, p_ghz = mfma_probe(torch)
+    res["mfma_probe"] = {"tflops": round(p_tf, 1), "sclk_ghz": round(p_ghz, 3),
+                         "attn_frac_of_probe": (round(res["roofline"]["achieved"] / p_tf, 4)
+                                                if res["roofline"]["bound"] == "mfma" else None)}
+    extras = [] if args.extras.strip().lower() in ("", "none") else [e.strip() for e in args.extras.split(",")]
+    if extras:
+        res["extra"] = {}
+        for name in extras:
+            if name == str(args.config):
+                continue
+            x = measure_wave(name, dev, None, None, args.max_splits)
+            res["extra"][x.pop("_name")] = {k: x[k] for k in ("value", "unit", "pct_peak", "ms_per_step", "steps",
+                                                             "warmup", "new_tokens_per_s", "attn_kernel_ms",
+                                                             "config", "roofline")}
+    if not args.no_cpu_baseline:
+        import workloads as wl
+        spec = res.pop("_spec")
+        fresh = wl.make_tensors(spec, seed=res.pop("_seed"), device=dev, poison=False)
+        res["cpu_baseline"] = cpu_baseline(spec, fresh)
+        del fresh
+    for k in [k for k in res if k.startswith("_")]:
+        res.pop(k)
+    print(json.dumps(res), flush=True)
+
+
+SEEDS = {"1": 1000, "2": 2000, "3": 3000, "4": 4000, "5": 5000, "6p": 6000}
+
+
+def measure_wave(name, dev, warmup, steps, max_splits=0, calib_mib=0) -> dict:
+    """Time whole steps (plan, upload, and per layer append + attention) of one wave and return the
+    JSON fields of its line.  The attention launches are timed with events on the launch stream."""
     import numpy as np
     import torch
     import paper_2609_35263_amd as wp
     import workloads as wl
 
-    wp.load_library()
-    dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
-    spec = wl.config(args.config)
+    spec = wl.config(name)
     layers = spec.layers
-    seed = {"1": 1000, "2": 2000, "3": 3000, "4": 4000, "5": 5000, "6p": 6000}.get(str(args.config), 7000)
+    seed = SEEDS.get(name, 7000)
     big = flops_alg(spec) > 1e12
     # layer tensors, resident in HBM; timing runs use zero-filled (not NaN) unused slots
-    per_layer = [wl.make_tensors(spec, seed=seed, device=dev if big else "cpu", poison=False, layer=l)
-                 for l in range(layers)]
-    cpu_layer0 = per_layer[0] if not big else None
-    dl = [{k: (None if v is None else v.to(dev).contiguous()) for k, v in t.items()} for t in per_layer]
+    dl = []
+    for l in range(layers):
+        t = wl.make_tensors(spec, seed=seed, device=dev if big else "cpu", poison=False, layer=l)
+        dl.append({k: (None if v is None else v.to(dev).contiguous()) for k, v in t.items()})
+        del t
     T = spec.total_tokens
     outs = [torch.empty((T, spec.num_q_heads, spec.head_dim_v), dtype=torch.bfloat16, device=dev)
             for _ in range(layers)]
     lses = [torch.empty((T, spec.num_q_heads), dtype=torch.float32, device=dev) for _ in range(layers)]
-    p0 = wp.plan_for(spec, max_splits=args.max_splits)
+    p0 = wp.plan_for(spec, max_splits=max_splits)
     ws = wp.new_workspace(p0, dev)
     info = p0.info()
     stream = torch.cuda.current_stream()
@@ -239,7 +309,7 @@ def main():
     attn_events = []
 
     def step(record=False):
-        p = wp.plan_for(spec, max_splits=args.max_splits)
+        p = wp.plan_for(spec, max_splits=max_splits)
         wp.plan_upload(p, ws)
         for l in range(layers):
             d = dl[l]
@@ -254,15 +324,15 @@ def main():
                 wp.chunked_prefill(p, d["q"], d["k_pool"], d["v_pool"], outs[l], lses[l], ws)
         return p
 
-    if args.copy_calibration_mib:
-        n = args.copy_calibration_mib << 20
+    if calib_mib:
+        n = calib_mib << 20
         src = torch.ones(n, dtype=torch.uint8, device=dev)
         dst = torch.empty_like(src)
         torch.cuda.synchronize()
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
-    warmup, steps, elapsed = run_timed(step, torch.cuda.synchronize, args.warmup, args.steps)
+    warmup, steps, elapsed = run_timed(step, torch.cuda.synchronize, warmup, steps)
     ms_per_step = elapsed * 1e3 / steps
     attn_all = [a.elapsed_time(b) for a, b in attn_events]
     attn_ms = float(np.mean(attn_all))
@@ -277,6 +347,7 @@ def main():
     a1.record(stream)
     torch.cuda.synchronize()
     append_ms = a0.elapsed_time(a1) / 5
+    del dl, outs, lses
 
     f_layer = flops_alg(spec)
     f_step = f_layer * layers
@@ -306,7 +377,7 @@ def main():
         roofline = {"bound": "hbm", "achieved": round(gbps, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                     "frac": round(gbps / PEAK_HBM_GBS, 4), "traffic": traffic, "kernel": kernel_name,
                     "alg_flop_per_launch": f_layer, "alg_bytes_per_launch": b_layer, **counters}
-    res = {
+    return {
         "metric": METRIC,
         "value": round(value, 3),
         "unit": "TFLOP/s",
@@ -335,17 +406,8 @@ def main():
         "attn_alg_GBps": round(bytes_alg(spec) / (attn_ms * 1e-3) / 1e9, 1),
         "work_items": info["num_items"],
         "roofline": roofline,
+        "_name": spec.name, "_spec": spec, "_seed": seed,
     }
-    # what the matrix cores sustain on this chip with random-bit operands (a power-limited clock), as
-    # context for the nominal peak; run after the timed region
-    p_tf, p_ghz = mfma_probe(torch)
-    res["mfma_probe"] = {"tflops": round(p_tf, 1), "sclk_ghz": round(p_ghz, 3),
-                         "attn_frac_of_probe": round(achieved / p_tf, 4) if roofline["bound"] == "mfma" else None}
-    if not args.no_cpu_baseline:
-        # the pools were appended to in place on the device; start from the generator's output again
-        fresh = cpu_layer0 if cpu_layer0 is not None else wl.make_tensors(spec, seed=seed, device=dev, poison=False)
-        res["cpu_baseline"] = cpu_baseline(spec, fresh)
-    print(json.dumps(res), flush=True)
 
 
 KDA_METRIC = "KDA chunked-prefill new tokens/s on 1 GPU; % of HBM peak"
@@ -373,11 +435,8 @@ def kda_cpu_baseline(spec, tensors, budget_s=12.0):
     all heads, n grown until one run takes about `budget_s`.  Reported in new tokens/s of the whole layer."""
     import oracle.kda as okda
     import workloads as wl
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:
-        threads = os.cpu_count() or 1
+    host = host_cpu_info()
+    threads = host["blas_threads"] or host["cpu_count"]
     c0 = int(spec.chunk_lens[0])
     n = 8
     while True:
@@ -759,7 +818,7 @@ def _pmc_pass(counters, config, calib_mib):
     d = tempfile.mkdtemp(prefix=f"wavepp_{counters[0].lower()}_", dir=os.environ.get("TMPDIR", "/tmp"))
     cmd = ["rocprofv3", "--pmc", *counters, "-f", "csv", "-d", d, "-o", "run", "--",
            sys.executable, os.path.abspath(__file__), "--config", str(config), "--steps", "2", "--warmup", "1",
-           "--no-cpu-baseline", "--copy-calibration-mib", str(calib_mib)]
+           "--no-cpu-baseline", "--extras", "none", "--copy-calibration-mib", str(calib_mib)]
     print("[traffic] " + " ".join(cmd), flush=True)
     res = subprocess.run(cmd, cwd=os.environ.get("TMPDIR", "/tmp"), timeout=300)
     rows = []
@@ -774,7 +833,8 @@ def _pmc_pass(counters, config, calib_mib):
 
 def measure_traffic(config, out_json, calib_mib=1024):
     """rocprofv3 counter passes over a short run of this config: FETCH_SIZE, then WRITE_SIZE (HBM
-    bytes), then MfmaUtil, then TCC_HIT_sum and TCC_MISS_sum (L2 hit rate).
+    bytes), then MfmaUtil, then TCC_HIT_sum and TCC_MISS_sum (L2 hit rate), then SQ_LDS_BANK_CONFLICT
+    and SQ_INSTS_LDS (LDS bank-conflict cycles and LDS instructions).
 
     Each byte counter is scaled by what it reads for one plain device copy of calib_mib MiB in the
     same process (known bytes / counted bytes), then averaged over the kernel's launches.  The GPU is
@@ -808,9 +868,16 @@ def measure_traffic(config, out_json, calib_mib=1024):
     miss = sum(float(r["Counter_Value"]) for r in rows if kname in r["Kernel_Name"] and r["Counter_Name"] == "TCC_MISS_sum")
     if hit + miss > 0:
         out["l2_hit_pct"] = 100.0 * hit / (hit + miss)
+    rows = _pmc_pass(["SQ_LDS_BANK_CONFLICT", "SQ_INSTS_LDS"], config, calib_mib)
+    for cname, key in (("SQ_LDS_BANK_CONFLICT", "lds_bank_conflict_cycles_per_launch"),
+                       ("SQ_INSTS_LDS", "lds_instructions_per_launch")):
+        v = [float(r["Counter_Value"]) for r in rows if kname in r["Kernel_Name"] and r["Counter_Name"] == cname]
+        if v:
+            out[key] = sum(v) / len(v)
     out["command"] = (f"python bench.py --config {config} --measure-traffic <out.json>  (rocprofv3 --pmc passes "
-                      f"FETCH_SIZE; WRITE_SIZE; MfmaUtil; TCC_HIT_sum TCC_MISS_sum, each over: python3 bench.py "
-                      f"--config {config} --steps 2 --warmup 1 --no-cpu-baseline --copy-calibration-mib {calib_mib})")
+                      f"FETCH_SIZE; WRITE_SIZE; MfmaUtil; TCC_HIT_sum TCC_MISS_sum; SQ_LDS_BANK_CONFLICT SQ_INSTS_LDS, each "
+                      f"over: python3 bench.py --config {config} --steps 2 --warmup 1 --no-cpu-baseline --extras none "
+                      f"--copy-calibration-mib {calib_mib})")
     with open(out_json, "w") as f:
         json.dump(out, f, indent=1)
     print(json.dumps(out), flush=True)

@@ -115,8 +115,15 @@ typedef struct {
 
 /* Validate the wave and build its work list: query-row tiles of (request, KV head), each
  * optionally split over key ranges, heaviest first and spread over the chip's L2 domains.
+ * Follows Design of WavePP, "Pipeline Scheduling" (a chunk is the span request, starting token,
+ * length, and a span whose positions the materialized cache does not back must fail rather than
+ * run: WAVEPP_EPOSITION) and Preliminaries, "Reuse" (ceil(n / B) blocks in pages that need not be
+ * contiguous: entries outside the pool are WAVEPP_ERANGE).  The equal-size-chunks-cost-differently
+ * remark of the same section is why items are costed by rows x visible keys.
  * max_splits: 0 = choose automatically, else the largest number of key ranges per tile (>= 1).
- * On success *out receives a new plan.  Host only: makes no HIP call. */
+ * On success *out receives a new plan (caller destroys it); on error *out is NULL, nothing was
+ * allocated and wavepp_last_error() names the offending request / block.  Host only: makes no
+ * HIP call, so it is safe on a thread without a device. */
 int wavepp_attn_plan(const wavepp_attn_shape* shape, const wavepp_batch* batch, int32_t max_splits,
                      wavepp_plan** out);
 
@@ -132,29 +139,44 @@ int wavepp_plan_get_info(const wavepp_plan* plan, wavepp_plan_info* info);
 int wavepp_plan_get_items(const wavepp_plan* plan, int32_t* items, int32_t capacity);
 
 /* Enqueue on `stream` the copy of the plan's metadata into the head of `workspace` (device
- * memory of at least wavepp_plan_workspace_bytes bytes, 256-byte aligned).  The source is a
- * library-owned pinned staging buffer, so the plan may be destroyed right after this returns; the
- * copy is a small kernel on `stream` that reads that buffer through its device mapping.
- * Kernels enqueued later on the same stream read the metadata from the workspace; a workspace
- * holding another plan's metadata makes them write nothing. */
+ * memory of at least wavepp_plan_workspace_bytes bytes, 256-byte aligned).  This is the
+ * "materialize before execute" step of Design of WavePP, "Decoupling Admission", for the wave's
+ * metadata.  The source is a library-owned pinned staging buffer, so the plan may be destroyed
+ * right after this returns; the copy is a small kernel on `stream` that reads that buffer through
+ * its device mapping.  The library records, per workspace address, which plan was uploaded last:
+ * wavepp_attn_append_kv and wavepp_attn_chunked_prefill return WAVEPP_EINVAL (and enqueue
+ * nothing) for a workspace whose last upload was of another plan or that had none.  The kernels
+ * also compare the plan's serial with the workspace header and write nothing on a mismatch (a
+ * workspace the caller overwrote after the upload).  Errors: WAVEPP_EINVAL (NULL / misaligned),
+ * WAVEPP_ENOSPACE (too small), WAVEPP_EHIP (staging allocation or launch failed). */
 int wavepp_attn_plan_upload(const wavepp_plan* plan, void* workspace, size_t ws_bytes, hipStream_t stream);
 
-/* Append (materialization).  Device pointers, bf16, row-major and contiguous:
+/* Append (materialization): the write of each chunk's K/V into the blocks reserved for positions
+ * [p_r, p_r + c_r) (A Minimum Implementation, steps 3-4; Decoupling Admission: freshly reserved
+ * suffix blocks are materialized before the chunk executes).  Device pointers, bf16, row-major
+ * and contiguous, owned by the caller:
  *   k_new [T][num_kv_heads][head_dim_qk], v_new [T][num_kv_heads][head_dim_v] (NULL if kv_shared)
  *   k_pool [num_pages][num_kv_heads][page_size][head_dim_qk], v_pool likewise (NULL if kv_shared)
  * Token cu_r + i is written to page block_table[r][(p_r + i) / B], slot (p_r + i) % B, for every
- * KV head; no other slot is touched.  The copy is bit-exact.  Requires a prior upload of `plan`
- * into `workspace` on this stream. */
+ * KV head; no other slot is touched.  The copy is bit-exact.  Requires that the last upload into
+ * `workspace` was of `plan` (else WAVEPP_EINVAL, nothing enqueued); WAVEPP_EINVAL also for NULL
+ * or non-16-byte-aligned buffers; WAVEPP_EHIP if the launch fails.  A wave with T = 0 is a no-op. */
 int wavepp_attn_append_kv(const wavepp_plan* plan, const void* k_new, const void* v_new, void* k_pool,
                           void* v_pool, void* workspace, size_t ws_bytes, hipStream_t stream);
 
-/* Attention.  Device pointers, row-major and contiguous:
+/* Attention of the wave's chunks: query i of chunk r attends to the whole cached prefix and to the
+ * chunk causally (Design of WavePP, "Waves and lanes": chunked prefill of the uncached suffix;
+ * Preliminaries, "Transformer Architectures": grouped and latent K/V sharing; "Reuse": paged
+ * blocks).  The definition is the one at the top of this file.  Device pointers, row-major and
+ * contiguous, owned by the caller:
  *   q [T][num_q_heads][head_dim_qk] bf16; pools as above (v_pool NULL if kv_shared), already
  *   holding the chunks' K/V (enqueue wavepp_attn_append_kv first on the same stream);
  *   out [T][num_q_heads][head_dim_v] bf16; lse [T][num_q_heads] fp32 or NULL.
  * Pool slots past p_r + c_r in a request's last page may hold any bits (NaN included); they do
- * not affect the result.  Requires a prior upload of `plan` into `workspace` on this stream.
- * Deterministic: repeated calls give bit-identical results. */
+ * not affect the result.  Requires that the last upload into `workspace` was of `plan` (else
+ * WAVEPP_EINVAL, nothing enqueued); WAVEPP_EINVAL also for NULL or misaligned buffers (16 bytes,
+ * lse 4); WAVEPP_EHIP if a launch fails.  Deterministic: repeated calls give bit-identical
+ * results. */
 int wavepp_attn_chunked_prefill(const wavepp_plan* plan, const void* q, const void* k_pool, const void* v_pool,
                                 void* out, float* lse, void* workspace, size_t ws_bytes, hipStream_t stream);
 

@@ -89,16 +89,18 @@ int wavepp_kda_get_info(const wavepp_kda_plan_t* plan, wavepp_kda_info* info);
 
 /* Enqueue on `stream` the copy of the plan's metadata into `workspace` (device memory of at least
  * wavepp_kda_workspace_bytes, 256-byte aligned) from a library-owned pinned buffer, by a small copy
- * kernel on `stream`. */
+ * kernel on `stream`.  The library records which plan each workspace address was given last (see
+ * wavepp_kda_chunked_prefill).  Errors: WAVEPP_EINVAL, WAVEPP_ENOSPACE, WAVEPP_EHIP. */
 int wavepp_kda_upload(const wavepp_kda_plan_t* plan, void* workspace, size_t ws_bytes, hipStream_t stream);
 
 /* Chunked prefill of one KDA layer.  Device pointers with the layouts above; q, k, v, alpha, beta,
  * state_pool and out 16-byte aligned.  Reads the snapshots named by state_in and writes out and
  * the snapshots named by state_out; every other slot and every other byte is left untouched.  A
- * snapshot slot that a request resumes from but does not write keeps its contents.  Requires a
- * prior upload of `plan` into `workspace` on this stream; a workspace holding another plan's
- * metadata makes the kernel write nothing.  Deterministic: repeated calls give bit-identical
- * results. */
+ * snapshot slot that a request resumes from but does not write keeps its contents (Preliminaries,
+ * "Reuse": a chunk resumes only from the exact snapshot of its prefix).  Requires that the last
+ * upload into `workspace` was of `plan`: otherwise WAVEPP_EINVAL and nothing is enqueued (the
+ * kernel also checks the plan's serial against the workspace header and writes nothing on a
+ * mismatch).  Deterministic: repeated calls give bit-identical results. */
 int wavepp_kda_chunked_prefill(const wavepp_kda_plan_t* plan, const void* q, const void* k, const void* v,
                                const float* alpha, const float* beta, float* state_pool, void* out,
                                void* workspace, size_t ws_bytes, hipStream_t stream);

@@ -273,9 +273,21 @@ def _stream(stream):
     return ctypes.c_void_p(s.cuda_stream)
 
 
-def _ptr(t, dtype=None, name=""):
+def _check_shapes(**named):
+    """Every tensor (name=(tensor or None, shape)) has the plan's shape.  Checked for all buffers of
+    a call before anything else: the kernels index every buffer by the plan's sizes, so a tensor of
+    any other shape would be read or written out of bounds."""
+    for name, (t, shape) in named.items():
+        if t is not None and tuple(t.shape) != tuple(int(x) for x in shape):
+            raise ValueError(f"{name} has shape {tuple(t.shape)}, the plan needs {tuple(int(x) for x in shape)}")
+
+
+def _ptr(t, dtype=None, name="", shape=None):
+    """Device pointer of a contiguous tensor of the given dtype and shape (None: no buffer)."""
     if t is None:
         return ctypes.c_void_p(None)
+    if shape is not None:
+        _check_shapes(**{name: (t, shape)})
     if not t.is_cuda:
         raise ValueError(f"{name} must be a device tensor")
     if not t.is_contiguous():
@@ -296,21 +308,46 @@ def plan_upload(p: Plan, workspace, stream=None):
                                                   workspace.numel() * workspace.element_size(), _stream(stream)))
 
 
+def _attn_shapes(p: Plan) -> dict:
+    s = p.shape
+    T, Hq, Hkv = s["total_tokens"], s["num_q_heads"], s["num_kv_heads"]
+    P, B, dq, dv = s["num_pages"], s["page_size"], s["head_dim_qk"], s["head_dim_v"]
+    return {"q": (T, Hq, dq), "k_new": (T, Hkv, dq), "v_new": (T, Hkv, dv), "k_pool": (P, Hkv, B, dq),
+            "v_pool": (P, Hkv, B, dv), "out": (T, Hq, dv), "lse": (T, Hq)}
+
+
+def _shared_kv_none(p: Plan, **bufs):
+    for name, t in bufs.items():
+        if p.shape["kv_shared"] and t is not None:
+            raise ValueError(f"{name} must be None for a latent (kv_shared) cache")
+        if not p.shape["kv_shared"] and t is None:
+            raise ValueError(f"{name} is required")
+
+
 def append_kv(p: Plan, k_new, v_new, k_pool, v_pool, workspace, stream=None):
     import torch
     bf = torch.bfloat16
+    sh = _attn_shapes(p)
+    _shared_kv_none(p, v_new=v_new, v_pool=v_pool)
+    _check_shapes(k_new=(k_new, sh["k_new"]), v_new=(v_new, sh["v_new"]), k_pool=(k_pool, sh["k_pool"]),
+                  v_pool=(v_pool, sh["v_pool"]))
     _check(load_library().wavepp_attn_append_kv(
-        p.handle, _ptr(k_new, bf, "k_new"), _ptr(v_new, bf, "v_new"), _ptr(k_pool, bf, "k_pool"),
-        _ptr(v_pool, bf, "v_pool"), _ptr(workspace, name="workspace"),
-        workspace.numel() * workspace.element_size(), _stream(stream)))
+        p.handle, _ptr(k_new, bf, "k_new", sh["k_new"]), _ptr(v_new, bf, "v_new", sh["v_new"]),
+        _ptr(k_pool, bf, "k_pool", sh["k_pool"]), _ptr(v_pool, bf, "v_pool", sh["v_pool"]),
+        _ptr(workspace, name="workspace"), workspace.numel() * workspace.element_size(), _stream(stream)))
 
 
 def chunked_prefill(p: Plan, q, k_pool, v_pool, out, lse, workspace, stream=None):
     import torch
     bf = torch.bfloat16
+    sh = _attn_shapes(p)
+    _shared_kv_none(p, v_pool=v_pool)
+    _check_shapes(q=(q, sh["q"]), k_pool=(k_pool, sh["k_pool"]), v_pool=(v_pool, sh["v_pool"]),
+                  out=(out, sh["out"]), lse=(lse, sh["lse"]))
     _check(load_library().wavepp_attn_chunked_prefill(
-        p.handle, _ptr(q, bf, "q"), _ptr(k_pool, bf, "k_pool"), _ptr(v_pool, bf, "v_pool"), _ptr(out, bf, "out"),
-        _ptr(lse, torch.float32, "lse"), _ptr(workspace, name="workspace"),
+        p.handle, _ptr(q, bf, "q", sh["q"]), _ptr(k_pool, bf, "k_pool", sh["k_pool"]),
+        _ptr(v_pool, bf, "v_pool", sh["v_pool"]), _ptr(out, bf, "out", sh["out"]),
+        _ptr(lse, torch.float32, "lse", sh["lse"]), _ptr(workspace, name="workspace"),
         workspace.numel() * workspace.element_size(), _stream(stream)))
 
 
@@ -384,9 +421,19 @@ def kda_upload(p: KdaPlan, workspace, stream=None):
 def kda_chunked_prefill(p: KdaPlan, q, k, v, alpha, beta, state_pool, out, workspace, stream=None):
     import torch
     bf, f32 = torch.bfloat16, torch.float32
+    s = p.shape
+    T, H, dk, dv = s["total_tokens"], s["num_heads"], s["head_dim_k"], s["head_dim_v"]
+    for name, t in (("q", q), ("k", k), ("v", v), ("alpha", alpha), ("beta", beta), ("state_pool", state_pool),
+                    ("out", out)):
+        if t is None:
+            raise ValueError(f"{name} is required")
+    _check_shapes(q=(q, (T, H, dk)), k=(k, (T, H, dk)), v=(v, (T, H, dv)), alpha=(alpha, (T, H, dk)),
+                  beta=(beta, (T, H)), state_pool=(state_pool, (s["num_state_slots"], H, dk, dv)),
+                  out=(out, (T, H, dv)))
     _check(load_library().wavepp_kda_chunked_prefill(
-        p.handle, _ptr(q, bf, "q"), _ptr(k, bf, "k"), _ptr(v, bf, "v"), _ptr(alpha, f32, "alpha"),
-        _ptr(beta, f32, "beta"), _ptr(state_pool, f32, "state_pool"), _ptr(out, bf, "out"),
+        p.handle, _ptr(q, bf, "q", (T, H, dk)), _ptr(k, bf, "k", (T, H, dk)), _ptr(v, bf, "v", (T, H, dv)),
+        _ptr(alpha, f32, "alpha", (T, H, dk)), _ptr(beta, f32, "beta", (T, H)),
+        _ptr(state_pool, f32, "state_pool", (s["num_state_slots"], H, dk, dv)), _ptr(out, bf, "out", (T, H, dv)),
         _ptr(workspace, name="workspace"), workspace.numel() * workspace.element_size(), _stream(stream)))
 
 

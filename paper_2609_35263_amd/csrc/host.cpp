@@ -20,6 +20,7 @@
 #include <mutex>
 #include <numeric>
 #include <string>
+#include <unordered_map>
 #include <vector>
 
 using namespace wavepp;
@@ -70,6 +71,40 @@ void clear_error() { g_last_error.clear(); }
 const char* last_error_text() { return g_last_error.c_str(); }
 
 uint32_t next_serial() { return g_serial.fetch_add(1); }
+
+// Which plan's metadata each workspace was last given, by the serial of the plan whose upload this
+// library enqueued into it.  The entry points that launch kernels consult it before enqueuing
+// anything, so a missing or stale upload is an error on the host; the kernels' own serial check
+// stays as a second guard (e.g. for a workspace the caller overwrote in between).
+namespace {
+std::mutex g_ws_mu;
+std::unordered_map<uintptr_t, uint32_t> g_ws_serial;
+}  // namespace
+
+void note_upload(const void* workspace, uint32_t serial) {
+  std::lock_guard<std::mutex> lock(g_ws_mu);
+  g_ws_serial[reinterpret_cast<uintptr_t>(workspace)] = serial;
+}
+
+int require_upload(const void* workspace, uint32_t serial, const char* upload_fn) {
+  uint32_t have = 0;
+  bool found = false;
+  {
+    std::lock_guard<std::mutex> lock(g_ws_mu);
+    auto it = g_ws_serial.find(reinterpret_cast<uintptr_t>(workspace));
+    if (it != g_ws_serial.end()) {
+      found = true;
+      have = it->second;
+    }
+  }
+  if (!found)
+    return set_error(WAVEPP_EINVAL, "workspace %p holds no uploaded plan: call %s(plan, workspace) first", workspace,
+                     upload_fn);
+  if (have != serial)
+    return set_error(WAVEPP_EINVAL, "workspace %p holds the metadata of another plan (serial %u, this plan %u): call "
+                     "%s(plan, workspace) first", workspace, have, serial, upload_fn);
+  return WAVEPP_OK;
+}
 
 }  // namespace wavepp
 
@@ -383,7 +418,9 @@ int wavepp_attn_plan(const wavepp_attn_shape* shape, const wavepp_batch* batch, 
   const bool small_rows = gw_n == 4 || (gw_n != 8 && max_rows <= kGqaRowsPerItem / 2);
   const int gqa_rows = small_rows ? kGqaRowsPerItem / 2 : kGqaRowsPerItem;
   const int M = mla ? kMlaRowsPerItem : gqa_rows;
-  const int KT = mla ? kMlaKvTile : kKvTile;
+  // keys per tile of the kernel that will run the plan (the 4-wave grouped form uses half tiles);
+  // split boundaries fall on whole tiles of it
+  const int KT = mla ? kMlaKvTile : (small_rows ? kKvTile / 2 : kKvTile);
   plan->rows_per_item = M;
   plan->kv_tile = KT;
 
@@ -411,8 +448,10 @@ int wavepp_attn_plan(const wavepp_attn_shape* shape, const wavepp_batch* batch, 
         base.push_back(w);
       }
   }
-  // key-range splits: forced by max_splits, or chosen so that a small wave still fills the chip
+  // key-range splits: forced by max_splits, or chosen so that a small wave still fills the chip,
+  // each automatic split keeping at least 1,024 keys (grouped kernel) or 512 (latent kernel)
   const int64_t fill_target = 1024;  // resident workgroups the chip can hold, x2
+  const int64_t min_split_tiles = (mla ? 512 : 1024) / KT;
   std::vector<WorkItem> items;
   int64_t part_rows = 0;
   int max_used = 1;
@@ -422,7 +461,7 @@ int wavepp_attn_plan(const wavepp_attn_shape* shape, const wavepp_batch* batch, 
     if (max_splits >= 1) {
       S = std::min<int64_t>(max_splits, ntiles);
     } else if (int64_t(base.size()) < fill_target / 2) {
-      S = std::min<int64_t>(ceil_div(fill_target, int64_t(base.size())), ntiles / 8);
+      S = std::min<int64_t>(ceil_div(fill_target, int64_t(base.size())), ntiles / min_split_tiles);
       S = std::max<int64_t>(S, 1);
     }
     const int64_t tps = ceil_div(ntiles, S);
@@ -532,7 +571,10 @@ int wavepp_attn_plan_upload(const wavepp_plan* plan, void* workspace, size_t ws_
   if (!plan) return set_error(WAVEPP_EINVAL, "plan is NULL");
   int st = check_workspace(plan, workspace, ws_bytes);
   if (st) return st;
-  return stage_and_copy(plan->blob.data(), plan->blob.size(), workspace, stream);
+  st = stage_and_copy(plan->blob.data(), plan->blob.size(), workspace, stream);
+  if (st) return st;
+  note_upload(workspace, plan->serial);
+  return WAVEPP_OK;
 }
 
 int wavepp_attn_append_kv(const wavepp_plan* plan, const void* k_new, const void* v_new, void* k_pool, void* v_pool,
@@ -543,6 +585,8 @@ int wavepp_attn_append_kv(const wavepp_plan* plan, const void* k_new, const void
   if (st) return st;
   const bool shared = plan->shape.kv_shared != 0;
   if (plan->total_tokens == 0) return WAVEPP_OK;
+  st = require_upload(workspace, plan->serial, "wavepp_attn_plan_upload");
+  if (st) return st;
   if (!k_new || !k_pool) return set_error(WAVEPP_EINVAL, "k_new / k_pool is NULL");
   if (!shared && (!v_new || !v_pool)) return set_error(WAVEPP_EINVAL, "v_new / v_pool is NULL");
   if (shared && (v_new || v_pool)) return set_error(WAVEPP_EINVAL, "v_new / v_pool must be NULL for a latent cache");
@@ -562,6 +606,8 @@ int wavepp_attn_chunked_prefill(const wavepp_plan* plan, const void* q, const vo
   if (st) return st;
   const bool shared = plan->shape.kv_shared != 0;
   if (plan->total_tokens == 0) return WAVEPP_OK;
+  st = require_upload(workspace, plan->serial, "wavepp_attn_plan_upload");
+  if (st) return st;
   if (!q || !k_pool || !out) return set_error(WAVEPP_EINVAL, "q / k_pool / out is NULL");
   if (!shared && !v_pool) return set_error(WAVEPP_EINVAL, "v_pool is NULL");
   if (shared && v_pool) return set_error(WAVEPP_EINVAL, "v_pool must be NULL for a latent cache");

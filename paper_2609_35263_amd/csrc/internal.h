@@ -123,6 +123,11 @@ void clear_error();
 const char* last_error_text();
 int stage_and_copy(const void* src, size_t bytes, void* dst, hipStream_t stream);
 uint32_t next_serial();
+// Record that `workspace` was given the metadata of the plan with this serial (on the caller's
+// stream); require_upload returns WAVEPP_EINVAL, with a last-error message naming upload_fn, when
+// the last upload into `workspace` was of another plan or there was none.
+void note_upload(const void* workspace, uint32_t serial);
+int require_upload(const void* workspace, uint32_t serial, const char* upload_fn);
 
 hipError_t launch_append(const DevPlan& p, const void* k_new, const void* v_new, void* k_pool, void* v_pool,
                          hipStream_t stream);

@@ -145,7 +145,10 @@ int wavepp_kda_upload(const wavepp_kda_plan_t* plan, void* workspace, size_t ws_
   if (!plan) return set_error(WAVEPP_EINVAL, "plan is NULL");
   int st = check_ws(plan, workspace, ws_bytes);
   if (st) return st;
-  return stage_and_copy(plan->blob.data(), plan->blob.size(), workspace, stream);
+  st = stage_and_copy(plan->blob.data(), plan->blob.size(), workspace, stream);
+  if (st) return st;
+  note_upload(workspace, plan->serial);
+  return WAVEPP_OK;
 }
 
 int wavepp_kda_chunked_prefill(const wavepp_kda_plan_t* plan, const void* q, const void* k, const void* v,
@@ -156,6 +159,8 @@ int wavepp_kda_chunked_prefill(const wavepp_kda_plan_t* plan, const void* q, con
   int st = check_ws(plan, workspace, ws_bytes);
   if (st) return st;
   if (plan->items.empty()) return WAVEPP_OK;
+  st = require_upload(workspace, plan->serial, "wavepp_kda_upload");
+  if (st) return st;
   if (!q || !k || !v || !alpha || !beta || !state_pool || !out)
     return set_error(WAVEPP_EINVAL, "q / k / v / alpha / beta / state_pool / out is NULL");
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(alpha) || !aligned16(beta) ||

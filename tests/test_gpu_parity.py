@@ -192,48 +192,120 @@ def test_wrong_workspace_or_small_workspace():
     with pytest.raises(wp.WaveppError) as e:
         wp.plan_upload(p, small)
     assert e.value.status == -6
-    # a workspace holding another plan's metadata: the kernels write nothing
+    # a workspace holding another plan's metadata: the host refuses the calls, nothing is enqueued
     other = wp.plan_for(spec, max_splits=2)
     ws = wp.new_workspace(p)
     wp.plan_upload(other, ws)
     out = torch.full((spec.total_tokens, 8, 64), 7.0, dtype=torch.bfloat16, device="cuda")
     d = {k: v.cuda() for k, v in t.items()}
+    with pytest.raises(wp.WaveppError) as e:
+        wp.chunked_prefill(p, d["q"], d["k_pool"], d["v_pool"], out, None, ws)
+    assert e.value.status == -1 and "wavepp_attn_plan_upload" in str(e.value)
+    with pytest.raises(wp.WaveppError) as e:
+        wp.append_kv(p, d["k_new"], d["v_new"], d["k_pool"], d["v_pool"], ws)
+    assert e.value.status == -1
+    torch.cuda.synchronize()
+    assert bool((out == 7.0).all())
+    # the kernels' own guard: the host map says this plan, but the workspace header was overwritten
+    # since (here by the other plan's metadata, copied in by the caller): the kernels write nothing
+    wp.plan_upload(p, ws)
+    ws2 = wp.new_workspace(other)
+    wp.plan_upload(other, ws2)
+    n = min(ws.numel(), ws2.numel())
+    ws[:n].copy_(ws2[:n])
     wp.chunked_prefill(p, d["q"], d["k_pool"], d["v_pool"], out, None, ws)
     torch.cuda.synchronize()
     assert bool((out == 7.0).all())
+    # and after a proper upload the same call runs
+    wp.plan_upload(p, ws)
+    wp.append_kv(p, d["k_new"], d["v_new"], d["k_pool"], d["v_pool"], ws)
+    wp.chunked_prefill(p, d["q"], d["k_pool"], d["v_pool"], out, None, ws)
+    torch.cuda.synchronize()
+    assert bool(torch.isfinite(out.float()).all())
 
 
 def test_sampled_rows_cfg3():
     sampled_config_check(wl.cfg3(), seed=3000)
 
 
-def test_sampled_rows_cfg4_layer():
-    sampled_config_check(wl.cfg4(), seed=4000)
-
-
-def test_sampled_rows_small_chunk_wave():
-    """16-token chunks over 16K-32K cached tokens: 128-row items, automatic key-range splits and the merge."""
-    sampled_config_check(wl.small_chunk(16), seed=7016)
-
-
-def sampled_config_check(spec, seed, rows_per_req=16, max_requests=None):
-    """Large configs: the full HIP path runs; the oracle recomputes sampled rows one by one."""
+def test_sampled_rows_cfg4_all_four_layers():
+    """The concurrency-128 wave as the bench runs it: one plan and one upload, then append and
+    attention for four layers with distinct pools, queries and outputs; sampled rows of every layer
+    against the oracle, and every layer's pools bit-exact."""
     torch = _torch()
-    say(f"[sampled] {spec.name} R={spec.num_requests} T={spec.total_tokens}")
-    t = wl.make_tensors(spec, seed=seed, device="cuda", poison=True)
-    # copies of the inputs the oracle needs, taken before the HIP path runs
+    import paper_2609_35263_amd as wp
+    spec = wl.cfg4()
+    assert spec.layers == 4
+    say(f"[layers] {spec.name} R={spec.num_requests} T={spec.total_tokens} layers={spec.layers}")
+    samples = sample_rows(spec, seed=4000)
+    p = wp.plan_for(spec)
+    ws = wp.new_workspace(p)
+    wp.plan_upload(p, ws)
+    layers, refs = [], []
+    for l in range(spec.layers):
+        t = wl.make_tensors(spec, seed=4000, device="cuda", poison=True, layer=l)
+        refs.append(oracle_rows(spec, t, samples))
+        out = torch.full((spec.total_tokens, spec.num_q_heads, spec.head_dim_v), float("nan"), dtype=torch.bfloat16,
+                         device="cuda")
+        lse = torch.full((spec.total_tokens, spec.num_q_heads), float("nan"), dtype=torch.float32, device="cuda")
+        layers.append((t, out, lse))
+    for t, out, lse in layers:
+        wp.append_kv(p, t["k_new"], t["v_new"], t["k_pool"], t["v_pool"], ws)
+        wp.chunked_prefill(p, t["q"], t["k_pool"], t["v_pool"], out, lse, ws)
+    torch.cuda.synchronize()
+    for l, ((t, out, lse), ref) in enumerate(zip(layers, refs)):
+        o = out_f64(out[samples[:, 0], samples[:, 1]])
+        ls = lse[samples[:, 0], samples[:, 1]].cpu().numpy()
+        rep = _compare.assert_parity(o, ref["o"], ls, ref["lse"], f"{spec.name} layer {l}")
+        assert bool(torch.isfinite(out.float()).all()), f"non-finite output in layer {l}"
+        assert np.array_equal(wl.to_bits(t["k_pool"]), ref["k_pool"]), f"K pool of layer {l}"
+        assert np.array_equal(wl.to_bits(t["v_pool"]), ref["v_pool"]), f"V pool of layer {l}"
+        say(f"  layer {l} parity {rep} over {len(samples)} rows")
+    # the layers differ: a kernel that read layer 0's pools for every layer would be caught here
+    assert not np.array_equal(refs[0]["o"], refs[1]["o"])
+
+
+def test_sampled_rows_cfg6p():
+    """The paper's 4K-suffix-behind-125K-prefix wave."""
+    sampled_config_check(wl.cfg6p(), seed=6000, rows_per_req=12)
+
+
+@pytest.mark.parametrize("chunk", [16, 32, 64, 128])
+def test_sampled_rows_small_chunk_wave(chunk):
+    """Short chunks over 16K-32K cached tokens (the gather-bound sweep): 128-row items with 64-key
+    tiles at c = 16, 256-row items beyond; automatic key-range splits and the merge."""
+    sampled_config_check(wl.small_chunk(chunk), seed=7000 + chunk)
+
+
+def sample_rows(spec, seed, rows_per_req=16, heads_per_row=4):
+    """(packed token, query head) rows of every request with a chunk: the first and last chunk token,
+    the tokens on either side of every page boundary the chunk crosses (at most 8 of them), and seeded
+    random tokens, each with `heads_per_row` random heads; plus one random token with every head."""
     rng = np.random.default_rng(seed)
     cu = spec.cu_tokens
-    samples = []
-    for r in range(spec.num_requests if max_requests is None else min(max_requests, spec.num_requests)):
-        c = int(spec.chunk_lens[r])
+    B = spec.page_size
+    samples = set()
+    for r in range(spec.num_requests):
+        p, c = int(spec.prefix_lens[r]), int(spec.chunk_lens[r])
         if c == 0:
             continue
-        toks = {0, c - 1, min(c - 1, 63), min(c - 1, 64)} | set(rng.integers(0, c, rows_per_req).tolist())
+        toks = {0, c - 1}
+        bounds = [i for i in range(c) if (p + i) % B == 0][:4]
+        for i in bounds:
+            toks |= {max(0, i - 1), i}
+        toks |= set(rng.integers(0, c, rows_per_req).tolist())
         for i in toks:
-            for h in rng.choice(spec.num_q_heads, 3, replace=False):
-                samples.append((int(cu[r]) + int(i), int(h)))
-    samples = np.array(sorted(set(samples)))
+            for h in rng.choice(spec.num_q_heads, min(heads_per_row, spec.num_q_heads), replace=False):
+                samples.add((int(cu[r]) + int(i), int(h)))
+        full = int(rng.integers(0, c))
+        for h in range(spec.num_q_heads):
+            samples.add((int(cu[r]) + full, h))
+    return np.array(sorted(samples))
+
+
+def oracle_rows(spec, t, samples):
+    """Oracle append (whole pools, bit patterns) and attention of the sampled rows, from copies of the
+    inputs taken before the HIP path runs."""
     q_rows = {int(tok): wl.to_bits(t["q"][int(tok)]) for tok in set(samples[:, 0].tolist())}
     pools_before = {k: wl.to_bits(t[k]) for k in ("k_pool", "v_pool") if t[k] is not None}
     new = {k: wl.to_bits(t[k]) for k in ("k_new", "v_new") if t[k] is not None}
@@ -243,13 +315,27 @@ def sampled_config_check(spec, seed, rows_per_req=16, max_requests=None):
                                                samples, page_size=spec.page_size, num_kv_heads=spec.num_kv_heads,
                                                softmax_scale=spec.softmax_scale, kv_shared=spec.kv_shared,
                                                head_dim_v=spec.head_dim_v)
+    return {"o": o_ref, "lse": l_ref, "k_pool": k1, "v_pool": v1}
+
+
+def sampled_config_check(spec, seed, rows_per_req=16, heads_per_row=4):
+    """Large configs: the full HIP path runs; the oracle recomputes sampled rows of every request."""
+    torch = _torch()
+    say(f"[sampled] {spec.name} R={spec.num_requests} T={spec.total_tokens}")
+    t = wl.make_tensors(spec, seed=seed, device="cuda", poison=True)
+    samples = sample_rows(spec, seed, rows_per_req, heads_per_row)
+    ref = oracle_rows(spec, t, samples)
     g = gpu_wave(spec, t)
     o = out_f64(g["out"][samples[:, 0], samples[:, 1]])
     lse = g["lse"][samples[:, 0], samples[:, 1]].cpu().numpy()
-    rep = _compare.assert_parity(o, o_ref, lse, l_ref, spec.name)
+    rep = _compare.assert_parity(o, ref["o"], lse, ref["lse"], spec.name)
     assert bool(torch.isfinite(g["out"].float()).all()), "non-finite output"
-    assert np.array_equal(wl.to_bits(g["k_pool"]), k1)
-    say(f"  parity {rep} over {len(samples)} rows")
+    assert np.array_equal(wl.to_bits(g["k_pool"]), ref["k_pool"])
+    if ref["v_pool"] is not None:
+        assert np.array_equal(wl.to_bits(g["v_pool"]), ref["v_pool"])
+    reqs = set(np.searchsorted(spec.cu_tokens, samples[:, 0], side="right") - 1)
+    say(f"  parity {rep} over {len(samples)} rows of {len(reqs)} requests")
+    return len(reqs)
 
 
 # ------------------------------------------------------------------------------------------
@@ -296,4 +382,6 @@ def test_latent_reference_overflow_takes_exact_second_pass():
 
 
 def test_sampled_rows_cfg5():
-    sampled_config_check(wl.cfg5(), seed=5000, rows_per_req=4, max_requests=2)
+    """The latent wave: sampled rows of all 8 requests (each over 139K visible keys)."""
+    n = sampled_config_check(wl.cfg5(), seed=5000, rows_per_req=8, heads_per_row=3)
+    assert n == 8

@@ -123,3 +123,39 @@ def test_tolerance_rejects_planted_mistakes(mistake):
                                     t["state_pool"].numpy(), [136], [-1], [1])
         o2 = np.concatenate([o_a, o_b])
     assert not _compare.kda_report(o2, o)["ok"], mistake
+
+
+# The same teeth at the size of one request of the measured KDA wave: a 4,096-token chunk resumed
+# from a snapshot, with heads spread over the decay rates the wave draws.  A mistake confined to one
+# 64-token block, or a decay applied one token late, must still fail the bar over the whole chunk.
+_WAVE_CASE = {}
+
+
+def _wave_case():
+    if not _WAVE_CASE:
+        spec = wk.custom(4, 128, 128, [4096], [0], [1], 2, name="kda_wave_request")
+        t = wk.make_tensors(spec, seed=4040)
+        bits = {n: wl.to_bits(t[n]) for n in ("q", "k", "v")}
+        o, _ = _run(bits, t)
+        _WAVE_CASE.update(spec=spec, t=t, bits=bits, o=o)
+    return _WAVE_CASE
+
+
+@pytest.mark.parametrize("mistake", ["decay_one_token_late", "block_dropped", "resume_from_zero"])
+def test_tolerance_rejects_planted_mistakes_at_wave_size(mistake):
+    case = _wave_case()
+    t, bits, o = case["t"], case["bits"], case["o"]
+    assert _compare.kda_scale(o) <= 1.5          # outputs of order one: the bar is (nearly) the unscaled one
+    alpha, beta = t["alpha"].numpy().copy(), t["beta"].numpy().copy()
+    if mistake == "decay_one_token_late":
+        # token t's state is decayed by alpha_{t-1} (the first token by none)
+        o2, _ = _run(bits, t, alpha=np.concatenate([np.ones_like(alpha[:1]), alpha[:-1]]))
+    elif mistake == "block_dropped":
+        # the updates of tokens 2048..2111 (one 64-token block in the middle) never reach the state
+        alpha[2048:2112] = 1.0
+        beta[2048:2112] = 0.0
+        o2, _ = _run(bits, t, alpha=alpha, beta=beta)
+    else:
+        o2, _ = _run(bits, t, state_in=(-1,))
+    rep = _compare.kda_report(o2, o)
+    assert not rep["ok"], (mistake, rep)

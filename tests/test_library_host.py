@@ -156,6 +156,32 @@ def test_item_rows_follow_the_largest_chunk(monkeypatch):
     coverage_check(wl.cfg2(), p.items(), p.info()["kv_tile"])
 
 
+def test_kv_tile_is_the_kernel_form_tile(monkeypatch):
+    """The 4-wave grouped form (128-row items) runs 64-key tiles and the 8-wave form 128-key tiles;
+    the plan reports the tile of the form it chose and splits on whole tiles of it."""
+    monkeypatch.delenv("WAVEPP_GQA_WAVES", raising=False)
+    small = wl.small_chunk(16)
+    ps = wp.plan_for(small)
+    assert ps.info()["rows_per_item"] == 128 and ps.info()["kv_tile"] == 64
+    coverage_check(small, ps.items(), 64)
+    for splits in (3, 7):
+        pf = wp.plan_for(small, max_splits=splits)
+        coverage_check(small, pf.items(), 64)
+        # forced splits cut at 64-key boundaries, so a split may start at an odd multiple of 64
+        assert pf.info()["kv_tile"] == 64
+    assert wp.plan_for(wl.cfg2()).info()["kv_tile"] == 128
+    # automatic splits keep at least 1,024 keys each, in either form
+    for spec in (small, wl.small_chunk(64), wl.cfg2()):
+        items = wp.plan_for(spec).items()
+        parts = items[(items[:, 6] >= 0) & (items[:, 3] > 0)]
+        if len(parts):
+            # every split but the last of its tile spans at least 1,024 keys
+            for (r, g, row0, rows, kb, ke, part, split) in parts:
+                later = parts[(parts[:, 0] == r) & (parts[:, 1] == g) & (parts[:, 2] == row0) & (parts[:, 7] > split)]
+                if len(later):
+                    assert ke - kb >= 1024, (r, g, row0, kb, ke)
+
+
 def test_plan_is_deterministic_and_independent_of_physical_pages():
     spec = wl.cfg2()
     a = wp.plan_for(spec).items()
@@ -184,3 +210,147 @@ def test_latent_plan_shapes():
     spec = wl.custom_wave(16, 1, 576, 512, 16, [37, 200, 5], [20, 1, 90], kv_shared=True, seed=1)
     for splits in (0, 2, 3):
         coverage_check(spec, wp.plan_for(spec, max_splits=splits).items(), 64)
+
+
+def _fake_call_args(p):
+    """Plausible-looking device addresses: these entry points must reject the call on the host,
+    before they look at the buffers, so nothing is ever dereferenced."""
+    return dict(ws=0x7f0000000000, ws_bytes=p.workspace_bytes + 4096)
+
+
+def test_missing_or_stale_upload_is_an_error_before_any_launch():
+    """append_kv and chunked_prefill refuse a workspace whose last upload was not this plan's (here:
+    none at all), with WAVEPP_EINVAL and a message naming the upload call; no HIP call is made."""
+    import ctypes
+    lib = wp.load_library()
+    p = wp.plan(**kw())
+    a = _fake_call_args(p)
+    vp = ctypes.c_void_p
+    buf = vp(0x7f0000100000)
+    st = lib.wavepp_attn_chunked_prefill(p.handle, buf, buf, buf, buf, None, vp(a["ws"]), a["ws_bytes"], None)
+    assert st == -1
+    assert b"wavepp_attn_plan_upload" in lib.wavepp_last_error()
+    st = lib.wavepp_attn_append_kv(p.handle, buf, buf, buf, buf, vp(a["ws"]), a["ws_bytes"], None)
+    assert st == -1
+    assert b"wavepp_attn_plan_upload" in lib.wavepp_last_error()
+    kp = wp.kda_plan(num_heads=2, head_dim_k=128, head_dim_v=128, num_state_slots=2, chunk_lens=[5],
+                     state_in=[-1], state_out=[0])
+    st = lib.wavepp_kda_chunked_prefill(kp.handle, buf, buf, buf, buf, buf, buf, buf, vp(a["ws"]),
+                                        kp.workspace_bytes + 4096, None)
+    assert st == -1
+    assert b"wavepp_kda_upload" in lib.wavepp_last_error()
+
+
+def test_binding_rejects_tensors_whose_shape_does_not_match_the_plan():
+    torch = pytest.importorskip("torch")
+    bf = torch.bfloat16
+    p = wp.plan(**kw())          # T = 32, Hq 8, Hkv 2, d 64, B 16, P 16
+    ws = torch.empty(p.workspace_bytes, dtype=torch.uint8)
+    good = dict(q=torch.empty(32, 8, 64, dtype=bf), k_pool=torch.empty(16, 2, 16, 64, dtype=bf),
+                v_pool=torch.empty(16, 2, 16, 64, dtype=bf), out=torch.empty(32, 8, 64, dtype=bf),
+                lse=torch.empty(32, 8, dtype=torch.float32))
+    bad = dict(q=torch.empty(31, 8, 64, dtype=bf), k_pool=torch.empty(15, 2, 16, 64, dtype=bf),
+               v_pool=torch.empty(16, 2, 16, 32, dtype=bf), out=torch.empty(32, 8, 32, dtype=bf),
+               lse=torch.empty(32, 4, dtype=torch.float32))
+    for name in good:
+        args = dict(good)
+        args[name] = bad[name]
+        with pytest.raises(ValueError, match="shape"):
+            wp.chunked_prefill(p, args["q"], args["k_pool"], args["v_pool"], args["out"], args["lse"], ws)
+    kn = torch.empty(32, 2, 64, dtype=bf)
+    with pytest.raises(ValueError, match="shape"):
+        wp.append_kv(p, kn[:31], kn, good["k_pool"], good["v_pool"], ws)
+    with pytest.raises(ValueError, match="shape"):
+        wp.append_kv(p, kn, kn, good["k_pool"], torch.empty(16, 2, 8, 64, dtype=bf), ws)
+    with pytest.raises(ValueError, match="required"):
+        wp.append_kv(p, kn, None, good["k_pool"], good["v_pool"], ws)
+    # right shapes, host memory: rejected as not on the device
+    with pytest.raises(ValueError, match="device"):
+        wp.chunked_prefill(p, good["q"], good["k_pool"], good["v_pool"], good["out"], good["lse"], ws)
+    kp = wp.kda_plan(num_heads=2, head_dim_k=128, head_dim_v=128, num_state_slots=3, chunk_lens=[5, 2],
+                     state_in=[-1, 0], state_out=[1, 2])
+    f32 = torch.float32
+    kgood = dict(q=torch.empty(7, 2, 128, dtype=bf), k=torch.empty(7, 2, 128, dtype=bf),
+                 v=torch.empty(7, 2, 128, dtype=bf), alpha=torch.empty(7, 2, 128, dtype=f32),
+                 beta=torch.empty(7, 2, dtype=f32), state_pool=torch.empty(3, 2, 128, 128, dtype=f32),
+                 out=torch.empty(7, 2, 128, dtype=bf))
+    for name, t in kgood.items():
+        args = dict(kgood)
+        args[name] = t[:-1]
+        with pytest.raises(ValueError, match="shape"):
+            wp.kda_chunked_prefill(kp, args["q"], args["k"], args["v"], args["alpha"], args["beta"],
+                                   args["state_pool"], args["out"], ws)
+
+
+def _expected_status(Hq, Hkv, dq, dv, B, P, kv_shared, prefix, chunk, bt):
+    """The validation rules of the plan, restated: shape, then each request in order (lengths,
+    span backed by the table, entries inside the pool), then pages receiving appended tokens must
+    be referenced exactly once among all entries that are read."""
+    if Hq % Hkv:
+        return -1
+    ok_dims = ((dq, dv) == (576, 512) and Hkv == 1) if kv_shared else (dq, dv) in ((64, 64), (128, 128))
+    if B not in (16, 64) or not ok_dims:
+        return -2
+    ref = np.zeros(P, np.int64)
+    for r in range(len(prefix)):
+        p, c = int(prefix[r]), int(chunk[r])
+        if p < 0 or c < 0:
+            return -1
+        if p + c > bt.shape[1] * B:
+            return -5
+        for b in range(-(-(p + c) // B)):
+            if not 0 <= bt[r, b] < P:
+                return -3
+            ref[bt[r, b]] += 1
+    for r in range(len(prefix)):
+        p, c = int(prefix[r]), int(chunk[r])
+        if c and any(ref[bt[r, b]] != 1 for b in range(p // B, -(-(p + c) // B))):
+            return -4
+    return 0
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_plan_fuzz_against_restated_rules(seed):
+    """Seeded random waves: random spans, shared / aliased / out-of-range / short block tables, head
+    shapes and forced splits.  The status must be the restated rules' status, and every accepted
+    plan's work list must cover every visible pair exactly once."""
+    rng = np.random.default_rng(100 + seed)
+    seen = set()
+    for _ in range(60):
+        shape = [(8, 2, 64, 64, False), (16, 4, 128, 128, False), (16, 1, 576, 512, True), (6, 4, 64, 64, False),
+                 (8, 2, 96, 96, False), (8, 1, 576, 512, False)][rng.integers(0, 6)]
+        Hq, Hkv, dq, dv, kv_shared = shape
+        B = int(rng.choice([16, 64, 16, 64, 32]))
+        P = int(rng.integers(1, 40))
+        R = int(rng.integers(0, 5))
+        stride = int(rng.integers(1, 9))
+        prefix = rng.integers(0, 150, R)
+        chunk = rng.integers(0, 120, R) * (rng.random(R) > 0.15)
+        if R and rng.random() < 0.05:
+            prefix[rng.integers(0, R)] = -1
+        if rng.random() < 0.6:
+            bt = np.resize(rng.permutation(P), (max(R, 1), stride)).astype(np.int32)[:R]
+        else:
+            bt = rng.integers(0, P, (R, stride)).astype(np.int32)
+        if R > 1 and rng.random() < 0.3:
+            bt[1, 0] = bt[0, 0]                      # a shared first page
+        if R and rng.random() < 0.1:
+            bt[rng.integers(0, R), rng.integers(0, stride)] = int(rng.choice([-1, P]))
+        bt = bt.reshape(R, stride)
+        want = _expected_status(Hq, Hkv, dq, dv, B, P, kv_shared, prefix, chunk, bt)
+        splits = int(rng.choice([0, 0, 1, 2, 5]))
+        try:
+            p = wp.plan(num_q_heads=Hq, num_kv_heads=Hkv, head_dim_qk=dq, head_dim_v=dv, page_size=B, num_pages=P,
+                        softmax_scale=0.1, prefix_lens=prefix, chunk_lens=chunk,
+                        block_table=bt if R else np.zeros((0, stride), np.int32), kv_shared=kv_shared,
+                        max_splits=splits)
+            got = 0
+        except wp.WaveppError as e:
+            got = e.status
+        assert got == want, (shape, B, P, prefix, chunk, bt)
+        seen.add(got)
+        if got == 0:
+            spec = wl.custom_wave(Hq, Hkv, dq, dv, B, prefix, chunk, kv_shared=kv_shared, num_pages=P, seed=1)
+            spec.block_table = bt
+            coverage_check(spec, p.items(), p.info()["kv_tile"])
+    assert 0 in seen

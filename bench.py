@@ -267,6 +267,7 @@ def main():
                                                              "config", "roofline")}
     if not args.no_cpu_baseline:
         import workloads as wl
+        progress("oracle baseline on the host cores")
         spec = res.pop("_spec")
         fresh = wl.make_tensors(spec, seed=res.pop("_seed"), device=dev, poison=False)
         res["cpu_baseline"] = cpu_baseline(spec, fresh)
@@ -277,6 +278,11 @@ def main():
 
 
 SEEDS = {"1": 1000, "2": 2000, "3": 3000, "4": 4000, "5": 5000, "6p": 6000}
+
+
+def progress(msg):
+    """A progress line on stderr (the JSON line alone goes to stdout)."""
+    print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
 
 
 def measure_wave(name, dev, warmup, steps, max_splits=0, calib_mib=0) -> dict:
@@ -332,8 +338,10 @@ def measure_wave(name, dev, warmup, steps, max_splits=0, calib_mib=0) -> dict:
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    progress(f"{spec.name}: inputs resident, {info['num_items']} work items; warm-up and timed steps")
     warmup, steps, elapsed = run_timed(step, torch.cuda.synchronize, warmup, steps)
     ms_per_step = elapsed * 1e3 / steps
+    progress(f"{spec.name}: {steps} timed steps after {warmup} warm-up, {ms_per_step:.3f} ms per step")
     attn_all = [a.elapsed_time(b) for a, b in attn_events]
     attn_ms = float(np.mean(attn_all))
 

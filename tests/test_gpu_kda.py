@@ -79,13 +79,26 @@ def test_kda_deterministic_and_stale_workspace():
     g2 = _harness.gpu_kda(spec, t)
     assert torch.equal(g1["out"].view(torch.int16), g2["out"].view(torch.int16))
     assert torch.equal(g1["state_pool"].view(torch.int32), g2["state_pool"].view(torch.int32))
-    # a workspace holding another plan's metadata: the kernel writes nothing
+    # a workspace holding another plan's metadata: the host refuses the call, nothing is enqueued
     other = wp.kda_plan_for(wk.custom(4, 128, 128, [5], [-1], [0], 10))
     ws = wp.new_workspace(g1["plan"])
     wp.kda_upload(other, ws)
     out = torch.zeros_like(g1["out"])
     pool = t["state_pool"].cuda().clone()
     d = g1["dev"]
+    with pytest.raises(wp.WaveppError) as e:
+        wp.kda_chunked_prefill(g1["plan"], d["q"], d["k"], d["v"], d["alpha"], d["beta"], pool, out, ws)
+    assert e.value.status == -1 and "wavepp_kda_upload" in str(e.value)
+    torch.cuda.synchronize()
+    assert not out.view(torch.int16).any()
+    assert torch.equal(pool.view(torch.int32), t["state_pool"].cuda().view(torch.int32))
+    # the kernel's own guard: the host map names this plan, but the caller overwrote the workspace
+    # header since (with the other plan's metadata): the kernel writes nothing
+    wp.kda_upload(g1["plan"], ws)
+    ws2 = wp.new_workspace(other)
+    wp.kda_upload(other, ws2)
+    n = min(ws.numel(), ws2.numel())
+    ws[:n].copy_(ws2[:n])
     wp.kda_chunked_prefill(g1["plan"], d["q"], d["k"], d["v"], d["alpha"], d["beta"], pool, out, ws)
     torch.cuda.synchronize()
     assert not out.view(torch.int16).any()

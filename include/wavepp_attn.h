@@ -180,6 +180,27 @@ int wavepp_attn_append_kv(const wavepp_plan* plan, const void* k_new, const void
 int wavepp_attn_chunked_prefill(const wavepp_plan* plan, const void* q, const void* k_pool, const void* v_pool,
                                 void* out, float* lse, void* workspace, size_t ws_bytes, hipStream_t stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc): the wave's append (if k_new is not NULL) and attention
+ * with no workspace argument and no allocation.  The plan's metadata and its split partials live in
+ * a static device array of the library, 160 MiB (167,772,160 bytes) per GPU, held from the first
+ * call on that GPU until the process ends; a plan whose wavepp_plan_workspace_bytes exceeds that is
+ * rejected with WAVEPP_ENOSPACE before anything is enqueued (plan it with a smaller max_splits).
+ * The metadata is copied from the plan's host memory with hipMemcpyAsync on `stream` (from
+ * pageable memory the runtime reads it before returning), then the same kernels as the
+ * workspace entry points run on `stream`; results are bit-identical to wavepp_attn_append_kv +
+ * wavepp_attn_chunked_prefill on the same plan.  Arguments as there: k_new / v_new as for
+ * wavepp_attn_append_kv (both NULL: the pools already hold the chunks' K/V; v_new NULL for a
+ * latent cache), q, pools, out, lse as for wavepp_attn_chunked_prefill.
+ * Every call on one GPU uses that GPU's one array: calls that overlap on one GPU (two streams, or
+ * a call enqueued before the previous call's kernels finished reading on another stream) race, and
+ * the array keeps the last call's contents.  Calls on one stream are ordered and safe.
+ * Errors: WAVEPP_EINVAL (NULL / misaligned buffers), WAVEPP_ENOSPACE (plan too large),
+ * WAVEPP_EHIP (symbol address, copy or launch failed). */
+int wavepp_attn_chunked_prefill_noalloc(const wavepp_plan* plan, const void* q, const void* k_new,
+                                        const void* v_new, void* k_pool, void* v_pool, void* out, float* lse,
+                                        hipStream_t stream);
+
 void wavepp_plan_destroy(wavepp_plan* plan);
 
 /* Static string for a status code. */

@@ -34,7 +34,7 @@ STATUS_NAMES = {0: "WAVEPP_OK", -1: "WAVEPP_EINVAL", -2: "WAVEPP_EUNSUPPORTED", 
 EXPORTED_SYMBOLS = [
     "wavepp_attn_plan", "wavepp_plan_workspace_bytes", "wavepp_plan_get_info", "wavepp_plan_get_items",
     "wavepp_attn_plan_upload", "wavepp_attn_append_kv", "wavepp_attn_chunked_prefill", "wavepp_plan_destroy",
-    "wavepp_status_string", "wavepp_last_error",
+    "wavepp_status_string", "wavepp_last_error", "wavepp_attn_chunked_prefill_noalloc",
 ]
 MPU_SYMBOLS = [
     "wavepp_mpu_budget_ladder", "wavepp_mpu_create", "wavepp_mpu_admit", "wavepp_mpu_plan", "wavepp_mpu_commit",
@@ -135,6 +135,8 @@ def load_library(path: str = None) -> ctypes.CDLL:
     lib.wavepp_attn_append_kv.restype = ctypes.c_int
     lib.wavepp_attn_chunked_prefill.argtypes = [vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.wavepp_attn_chunked_prefill.restype = ctypes.c_int
+    lib.wavepp_attn_chunked_prefill_noalloc.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp]
+    lib.wavepp_attn_chunked_prefill_noalloc.restype = ctypes.c_int
     lib.wavepp_plan_destroy.argtypes = [vp]
     lib.wavepp_plan_destroy.restype = None
     lib.wavepp_status_string.argtypes = [ctypes.c_int]
@@ -349,6 +351,23 @@ def chunked_prefill(p: Plan, q, k_pool, v_pool, out, lse, workspace, stream=None
         _ptr(v_pool, bf, "v_pool", sh["v_pool"]), _ptr(out, bf, "out", sh["out"]),
         _ptr(lse, torch.float32, "lse", sh["lse"]), _ptr(workspace, name="workspace"),
         workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def chunked_prefill_noalloc(p: Plan, q, k_pool, v_pool, out, lse, k_new=None, v_new=None, stream=None):
+    """Append (when k_new is given) and attention with no workspace: the library's static per-GPU
+    scratch holds the metadata and split partials.  Calls on one GPU must not overlap."""
+    import torch
+    bf = torch.bfloat16
+    sh = _attn_shapes(p)
+    _shared_kv_none(p, v_pool=v_pool)
+    if p.shape["kv_shared"] and v_new is not None:
+        raise ValueError("v_new must be None for a latent (kv_shared) cache")
+    _check_shapes(q=(q, sh["q"]), k_new=(k_new, sh["k_new"]), v_new=(v_new, sh["v_new"]),
+                  k_pool=(k_pool, sh["k_pool"]), v_pool=(v_pool, sh["v_pool"]), out=(out, sh["out"]),
+                  lse=(lse, sh["lse"]))
+    _check(load_library().wavepp_attn_chunked_prefill_noalloc(
+        p.handle, _ptr(q, bf, "q"), _ptr(k_new, bf, "k_new"), _ptr(v_new, bf, "v_new"), _ptr(k_pool, bf, "k_pool"),
+        _ptr(v_pool, bf, "v_pool"), _ptr(out, bf, "out"), _ptr(lse, torch.float32, "lse"), _stream(stream)))
 
 
 # ------------------------------------------------------------------------------------------------

@@ -624,6 +624,46 @@ int wavepp_attn_chunked_prefill(const wavepp_plan* plan, const void* q, const vo
   return WAVEPP_OK;
 }
 
+int wavepp_attn_chunked_prefill_noalloc(const wavepp_plan* plan, const void* q, const void* k_new,
+                                        const void* v_new, void* k_pool, void* v_pool, void* out, float* lse,
+                                        hipStream_t stream) {
+  clear_error();
+  if (!plan) return set_error(WAVEPP_EINVAL, "plan is NULL");
+  if (plan->workspace_bytes > kNoAllocScratchBytes)
+    return set_error(WAVEPP_ENOSPACE, "plan needs %zu bytes of scratch, the static scratch holds %zu: plan the wave "
+                     "with fewer key-range splits (max_splits) or call wavepp_attn_chunked_prefill with a workspace",
+                     plan->workspace_bytes, kNoAllocScratchBytes);
+  const bool shared = plan->shape.kv_shared != 0;
+  if (plan->total_tokens == 0) return WAVEPP_OK;
+  if (!q || !k_pool || !out) return set_error(WAVEPP_EINVAL, "q / k_pool / out is NULL");
+  if (!shared && !v_pool) return set_error(WAVEPP_EINVAL, "v_pool is NULL");
+  if (shared && (v_pool || v_new)) return set_error(WAVEPP_EINVAL, "v_pool / v_new must be NULL for a latent cache");
+  if (k_new && !shared && !v_new) return set_error(WAVEPP_EINVAL, "v_new is NULL while k_new is given");
+  if (!k_new && v_new) return set_error(WAVEPP_EINVAL, "v_new is given without k_new");
+  if (!aligned16(q) || !aligned16(k_pool) || !aligned16(out) || (!shared && !aligned16(v_pool)) ||
+      (k_new && !aligned16(k_new)) || (v_new && !aligned16(v_new)) || (reinterpret_cast<uintptr_t>(lse) & 3))
+    return set_error(WAVEPP_EINVAL, "device buffers must be 16-byte aligned (lse 4-byte)");
+  void* ws = nullptr;
+  hipError_t e = noalloc_scratch(&ws);
+  if (e != hipSuccess) return set_hip_error(e, "static scratch address");
+  // the plan's metadata into the head of the scratch (from the plan's own host memory: no staging
+  // buffer of the library's is involved), then the same kernels as the workspace entry points
+  e = hipMemcpyAsync(ws, plan->blob.data(), plan->blob.size(), hipMemcpyHostToDevice, stream);
+  if (e != hipSuccess) return set_hip_error(e, "metadata copy into the static scratch");
+  DevPlan d = make_dev(plan, ws);
+  if (k_new) {
+    e = launch_append(d, k_new, v_new, k_pool, v_pool, stream);
+    if (e != hipSuccess) return set_hip_error(e, "append_kv launch");
+  }
+  e = launch_attention(d, q, k_pool, v_pool, out, lse, stream);
+  if (e != hipSuccess) return set_hip_error(e, "attention launch");
+  if (!plan->merges.empty()) {
+    e = launch_merge(d, out, lse, stream);
+    if (e != hipSuccess) return set_hip_error(e, "merge launch");
+  }
+  return WAVEPP_OK;
+}
+
 void wavepp_plan_destroy(wavepp_plan* plan) { delete plan; }
 
 }  // extern "C"

@@ -138,4 +138,9 @@ hipError_t launch_merge(const DevPlan& p, void* out, float* lse, hipStream_t str
 // memory to device memory with a kernel on `stream`.
 hipError_t launch_upload(const void* src, void* dst, size_t bytes, hipStream_t stream);
 
+// Size of the static per-device scratch array of the allocation-free entry point, and the device
+// address of the current device's copy (taken with hipGetSymbolAddress on first use per device).
+constexpr size_t kNoAllocScratchBytes = size_t(160) << 20;
+hipError_t noalloc_scratch(void** ptr);
+
 }  // namespace wavepp

@@ -28,6 +28,7 @@
 #include "internal.h"
 
 #include <algorithm>
+#include <mutex>
 
 namespace wavepp {
 
@@ -856,6 +857,38 @@ hipError_t launch_merge(const DevPlan& p, void* out, float* lse, hipStream_t str
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------------------------
+// Scratch of the allocation-free entry point (wavepp_attn_chunked_prefill_noalloc): the plan's
+// metadata and its split partials live in this static device array instead of a caller workspace.
+// Each GPU the library runs on holds its own copy until the process ends.  In host code the name
+// `scratch` is only a host-side stand-in: its device address is taken once per device with
+// hipGetSymbolAddress and only that address is handed to kernels and copies.
+// ---------------------------------------------------------------------------------------------
+__device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+hipError_t noalloc_scratch(void** ptr) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));   // the current device's copy of the array
+    if (e != hipSuccess) return e;
+    if (!p || reinterpret_cast<uintptr_t>(p) % 256) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return hipSuccess;
 }
 
 }  // namespace wavepp

@@ -354,3 +354,20 @@ def test_plan_fuzz_against_restated_rules(seed):
             spec.block_table = bt
             coverage_check(spec, p.items(), p.info()["kv_tile"])
     assert 0 in seen
+
+
+def test_noalloc_entry_point_rejects_plans_beyond_its_static_scratch():
+    """The allocation-free entry point checks the plan's scratch need against its fixed 160 MiB array
+    before any HIP call."""
+    import ctypes
+    lib = wp.load_library()
+    spec = wl.small_chunk(128)
+    p = wp.plan_for(spec, max_splits=64)
+    assert p.workspace_bytes > 160 << 20
+    vp = ctypes.c_void_p
+    buf = vp(0x7f0000100000)
+    st = lib.wavepp_attn_chunked_prefill_noalloc(p.handle, buf, None, None, buf, buf, buf, None, None)
+    assert st == -6
+    assert b"static scratch" in lib.wavepp_last_error()
+    # a plan that fits passes the size check (and then needs a GPU: not called here)
+    assert wp.plan_for(spec).workspace_bytes <= 160 << 20

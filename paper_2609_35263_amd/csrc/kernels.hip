@@ -390,34 +390,62 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_gqa_kernel(DevP
 // Latent attention in absorbed form: every query head attends over one shared 576-wide latent per
 // token (keys = the whole latent, values = its first 512 lanes).  Page size PAGE (16 or 64).
 //
-// One workgroup = 4 waves (one per SIMD) = 64 query rows; latent tiles of 64 keys.  Logits: wave w
-// computes S^T for key block w/2 (32 keys) and row block w%2 (32 rows), 36 MFMAs with its 32 Q rows
-// in registers; the two waves sharing a row block exchange their row maxima through LDS and apply
-// identical softmax decisions.  Values: wave w accumulates O for all 64 rows on value lanes
-// [128w, 128w + 128), so each latent element is read from LDS by one wave for the values and by two
-// for the keys.  The bf16 probabilities, already in MFMA B-operand order, pass through LDS.
+// One workgroup = 4 waves (one per SIMD) = 64 query rows; latent tiles of 64 keys.
+//   * Logits: wave w computes S^T for key block w / 2 (32 keys) and row block w % 2 (32 rows), 36
+//     MFMAs with its 32 Q rows in registers.
+//   * Softmax reference: fixed per row at the item's first tile (both waves of a row block take
+//     the maximum over the tile's 64 keys, exchanged once through LDS) and never moved, so the
+//     accumulators are never rescaled and no maximum is exchanged afterwards.  If a later logit
+//     exceeds the reference by more than 2^64 the workgroup redoes its key range with the exact
+//     row maxima (tracked per lane, combined at the end).
+//   * Values: the bf16 probabilities, already in MFMA B-operand order, go through LDS; wave w
+//     accumulates O for all 64 rows on value lanes [128w, 128w + 128), so each transposed V
+//     fragment read from LDS feeds two MFMAs.
+//   * The next latent tile is copied global -> LDS by the DMA path (global_load_lds, 16 bytes per
+//     lane), issued at the start of a tile into the other of two buffers; no registers stage it.
+//     The two buffers are distinct LDS objects, and the current and next buffer pointers select
+//     between them on the same condition, so the compiler can tell that the DMAs never touch the
+//     buffer being read: reads of the current buffer do not wait for the DMAs in flight.  The barrier between the probability writes and
+//     the P.V reads only orders LDS accesses (the DMAs stay in flight); the barrier at the end of
+//     a tile waits for them.
+//   * Layout of a tile in LDS: 64 rows of 72 16-byte chunks, unpadded; chunk c of row j is stored
+//     at chunk position c ^ swz(j) of that row.  The swizzle puts the 16 rows read together by a
+//     K fragment load, and the 4 rows x 4 chunks read together by a transposed V load, on distinct
+//     banks.
 // ---------------------------------------------------------------------------------------------
+namespace mla {
+constexpr int DQ = 576, DV = 512, KT = 64;
+constexpr int CPR = DQ / 8;                  // 16-byte chunks per latent row (72)
+constexpr int ROW_BYTES = DQ * 2;            // 1152
+constexpr int TILE_BYTES = KT * ROW_BYTES;   // 73728
+constexpr int NDMA = KT * CPR / 64 / 4;      // DMA instructions (64 lanes x 16 bytes) per wave per tile: 18
+static_assert(NDMA * 4 * 64 == KT * CPR, "tile covered exactly by the DMA instructions");
+static_assert(kMlaRowsPerItem == 64 && kMlaKvTile == KT, "planner and kernel agree");
+// chunk position of logical chunk c of row j: c ^ swz(j) (swz < 8 keeps it in c's aligned group of 8)
+__device__ __forceinline__ uint32_t swz(uint32_t j) { return (((j >> 1) & 1u) << 2) | ((j >> 2) & 3u); }
+}  // namespace mla
+
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) unsigned char lds_u8;
+typedef __attribute__((address_space(3))) const bf16x8 lds_bf16x8;
+
+// Barrier for LDS data only: this wave's LDS reads and writes have completed, then the workgroup
+// meets.  Unlike __syncthreads() it does not wait for the wave's outstanding DMA loads into LDS.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0); vector-memory and export counts left unwaited
+  asm volatile("s_barrier" ::: "memory");
+}
+
 template <int PAGE>
 __global__ __launch_bounds__(256, 1) void attn_mla_kernel(DevPlan p, const __bf16* __restrict__ q,
                                                           const __bf16* __restrict__ lat, __bf16* __restrict__ out,
                                                           float* __restrict__ lse_out) {
-  constexpr int DQ = 576, DV = 512;
-  constexpr int KT = kMlaKvTile;        // 64 keys per tile
-  constexpr int STR = DQ + 8;           // latent rows in LDS (elements)
-  constexpr int CH = DQ / 8;            // 16-byte chunks per latent row
-  constexpr int LOADS = KT * CH / 256;  // chunks per thread per tile (18)
-  constexpr int PPT = (PAGE >= KT) ? 1 : KT / PAGE;
-  // The next tile is staged in NR rounds of registers.  Two rounds, each landing behind an MFMA phase
-  // (logits, then P V); with 16-token pages the page selection needs more registers, and a third,
-  // shorter round behind the softmax keeps that instantiation's spills down.
-  constexpr int NR = PPT == 1 ? 2 : 3;
-  constexpr int ROUND = LOADS / NR;
-  constexpr int DW = DV / 4;            // value lanes per wave
-  static_assert(LOADS * 256 == KT * CH && ROUND * NR == LOADS, "tile covered exactly");
-  __shared__ __attribute__((aligned(16))) __bf16 lt[2][KT * STR];
-  __shared__ __attribute__((aligned(16))) bf16x8 pl[2][4][64];   // [row block][16-key step][lane]
-  __shared__ float xm[2][2][32];                                 // [key block][row block][row]: partial max
-  __shared__ int ovf;                                            // some row exceeded its softmax reference
+  using namespace mla;
+  constexpr int PPT = (PAGE >= KT) ? 1 : KT / PAGE;   // pages per tile
+  __shared__ __attribute__((aligned(1024))) unsigned char lt0[TILE_BYTES];
+  __shared__ __attribute__((aligned(1024))) unsigned char lt1[TILE_BYTES];
+  __shared__ __attribute__((aligned(16))) bf16x8 pbuf[2][4][64];   // [row block][16-key step][lane]
+  __shared__ float xch[2][2][32];                                  // [key block][row block][row]
 
   if (!meta_ok(p)) return;
   const WorkItem it = p.items[blockIdx.x];
@@ -431,195 +459,230 @@ __global__ __launch_bounds__(256, 1) void attn_mla_kernel(DevPlan p, const __bf1
   const int32_t* __restrict__ bt = p.bt + rm.bt_row;
   const int64_t page_stride = int64_t(PAGE) * DQ;
 
-  // ---- this lane's S row -------------------------------------------------------------------------
+  // ---- this lane's logit row: row block rb; rows past it.rows repeat row 0 (never written) ------
   const int lrow = rb * 32 + col;
   const bool row_ok = lrow < it.rows;
   const int prow = it.row0 + (row_ok ? lrow : 0);
   const int tok = prow / G;
-  const int head = prow - tok * G;
   const int limit = rm.prefix + tok;
   bf16x8 qf[DQ / 16];
   {
-    const __bf16* qrow = q + (int64_t(rm.cu + tok) * Hq + head) * DQ + 8 * hf;
+    const __bf16* qrow = q + (int64_t(rm.cu + tok) * Hq + (prow - tok * G)) * DQ + 8 * hf;
 #pragma unroll
-    for (int s = 0; s < DQ / 16; ++s) qf[s] = row_ok ? *reinterpret_cast<const bf16x8*>(qrow + 16 * s) : bf16x8{};
+    for (int s = 0; s < DQ / 16; ++s) qf[s] = *reinterpret_cast<const bf16x8*>(qrow + 16 * s);
   }
-  const int blk_min_lim = rm.prefix + (it.row0 + 32 * rb) / G;
-
-  f32x16 oacc[2][DW / 32];              // [row block][value block]
-#pragma unroll
-  for (int r2 = 0; r2 < 2; ++r2)
-#pragma unroll
-    for (int db = 0; db < DW / 32; ++db) oacc[r2][db] = f32x16{};
-  float l_part = 0.0f;                  // this wave's key half of the row sum
+  // smallest limit among the row block's lanes (lanes past it.rows use row 0's limit)
+  const int blk_min_lim = rm.prefix + (it.row0 + ((rb * 32 + 32 <= it.rows) ? rb * 32 : 0)) / G;
   const float sl2 = p.softmax_scale * kLog2e;
+  const int bound_base = min(limit, it.kv_end - 1) - 32 * kb - 4 * hf;
 
-  // ---- latent tile staging -----------------------------------------------------------------------
+  // ---- per-lane LDS byte offsets ---------------------------------------------------------------
+  // K fragment of step s = 4a + b: row 32kb + col, chunk 2s + hf -> kofs[b] + 128a
+  // (the swizzle has period 16 in the row)
+  int kofs[4];
+#pragma unroll
+  for (int b = 0; b < 4; ++b)
+    kofs[b] = (32 * kb + col) * ROW_BYTES + 16 * int((2u * b + hf) ^ swz(uint32_t(col)));
+  // transposed V fragment of step t (16 keys), value block db (32 lanes of d), half lo/hi:
+  //   rows 16t + 4hf + (lane & 15) / 4 (+8 for hi), d = 128 wave + 32 db + 16 g + 4 (lane & 3)
+  //   -> (db even ? va : vb) + 128 (db >> 1) + 18432 t (+ dhi for hi)
+  int va, vb, dhi;
+  {
+    const int g = (lane >> 4) & 1;
+    const int j = 4 * hf + (lane & 15) / 4;
+    const int fj = int(swz(uint32_t(j)));
+    const int cf = (16 * wave + 2 * g + ((lane & 3) >> 1)) ^ fj;
+    const int fb2 = (fj >> 2) & 1;
+    const int x = j * ROW_BYTES + 16 * cf - 64 * fb2 + 8 * (lane & 1);
+    va = x + 64 * fb2;
+    vb = x + 64 * (1 - fb2);
+    dhi = 8 * ROW_BYTES + (((cf >> 1) & 1) ? -32 : 32);
+  }
+
+  // ---- DMA of one latent tile into an LDS buffer ------------------------------------------------
+  // Instruction i of wave w writes chunk positions P = 64 (w + 4i) + l (lane l) of the buffer; the
+  // position holds logical chunk (P % 72) ^ swz(P / 72) of row P / 72, i.e. the tile's bytes at
+  // 16 P + 16 d_i, where d_i = ((P % 8) ^ swz(P / 72)) - P % 8 lies in [-7, 7].  For whole tiles of
+  // 64-token pages (the tile is one page) a lane keeps 16 P_0 and the 18 values 16 d_i packed in
+  // bytes, so an instruction's source offset costs two ALU operations.  Other tiles (the request's
+  // last, partial one, or 16-token pages) compute row and chunk directly; rows past the request's
+  // last valid position copy that position's row (finite; the mask gives them zero weight), so
+  // stale or NaN pool slots are never read.
   const int last_block = (n_valid - 1) / PAGE;
-  u32x4 sreg[ROUND];
-  int pg_nxt[PPT];
-#define WAVEPP_MLA_PAGES(tile_, pg_)                                                                      \
-  _Pragma("unroll") for (int i_ = 0; i_ < PPT; ++i_) pg_[i_] = bt[min((tile_) * (KT / PAGE) + i_, last_block)];
-#define WAVEPP_MLA_LOAD(tile_, pg_, i0_)                                                                  \
-  {                                                                                                       \
-    const int kbase_ = (tile_) * KT;                                                                      \
-    _Pragma("unroll") for (int i_ = 0; i_ < ROUND; ++i_) {                                                \
-      const int c_ = tid + 256 * ((i0_) + i_);                                                            \
-      const int j_ = min(kbase_ + c_ / CH, n_valid - 1);                                                  \
-      int page_ = pg_[0];                                                                                 \
-      _Pragma("unroll") for (int q_ = 1; q_ < PPT; ++q_) page_ = ((j_ - kbase_) / PAGE == q_) ? pg_[q_] : page_; \
-      sreg[i_] = *reinterpret_cast<const u32x4*>(lat + int64_t(page_) * page_stride +                     \
-                                                 (uint32_t(j_ % PAGE) * DQ + uint32_t(c_ % CH) * 8));     \
-    }                                                                                                     \
+  const int wave_s = __builtin_amdgcn_readfirstlane(wave);
+  const uint32_t dma_o0 = 16u * uint32_t(64 * wave + lane);
+  uint32_t dma_d[(NDMA + 3) / 4] = {};
+#pragma unroll
+  for (int i = 0; i < NDMA; ++i) {
+    const uint32_t P = uint32_t(64 * (wave + 4 * i) + lane);
+    const int q7 = int(P % CPR) & 7;
+    const int d = ((q7 ^ int(swz(P / CPR))) - q7) * 16;
+    dma_d[i / 4] |= (uint32_t(d) & 0xFFu) << (8 * (i % 4));
   }
-#define WAVEPP_MLA_STORE(buf_, i0_)                                                                       \
-  _Pragma("unroll") for (int i_ = 0; i_ < ROUND; ++i_) {                                                  \
-    const int c_ = tid + 256 * ((i0_) + i_);                                                              \
-    *reinterpret_cast<u32x4*>(&lt[buf_][(c_ / CH) * STR + (c_ % CH) * 8]) = sreg[i_];                     \
-  }
+  auto dma_tile = [&](lds_u8* buf, int tile) {
+    const int kbase = tile * KT;
+    if (PAGE >= KT && kbase + KT <= n_valid) {
+      const char* tbase = reinterpret_cast<const char*>(lat + int64_t(bt[tile]) * page_stride);
+#pragma unroll
+      for (int i = 0; i < NDMA; ++i) {
+        const int d = int(dma_d[i / 4] << (24 - 8 * (i % 4))) >> 24;
+        __builtin_amdgcn_global_load_lds(tbase + (dma_o0 + 4096u * i + d), (lds_void*)(buf + 1024 * (wave_s + 4 * i)),
+                                         16, 0, 0);
+      }
+      return;
+    }
+    const uint32_t jmax = uint32_t(n_valid - 1 - kbase);
+    int pg[PPT];
+#pragma unroll
+    for (int i = 0; i < PPT; ++i) pg[i] = bt[min(tile * (KT / PAGE) + i, last_block)];
+#pragma unroll
+    for (int i = 0; i < NDMA; ++i) {
+      const uint32_t P = uint32_t(64 * (wave + 4 * i) + lane);
+      const uint32_t j = P / CPR;
+      const uint32_t c = (P - CPR * j) ^ swz(j);
+      const uint32_t je = min(j, jmax);
+      int page = pg[0];
+#pragma unroll
+      for (int u = 1; u < PPT; ++u) page = (je / PAGE == uint32_t(u)) ? pg[u] : page;
+      __builtin_amdgcn_global_load_lds(lat + int64_t(page) * page_stride + ((je % PAGE) * DQ + 8 * c),
+                                       (lds_void*)(buf + 1024 * (wave_s + 4 * i)), 16, 0, 0);
+    }
+  };
 
-  const int k_lane = (32 * kb + col) * STR + 8 * hf;
-  const int v_lane = (4 * hf + (lane & 15) / 4) * STR + 16 * ((lane >> 4) & 1) + 4 * (lane & 3) + DW * wave;
-
+  f32x16 oacc[2][4];                    // [row block][value block]: O^T for value lanes 128 wave + 32 db
+  float l_lane = 0.0f;                  // this lane's part of its row's sum (its key block, its half)
+  float m_ref = -INFINITY;              // row reference (log2 units, scaled), equal in both key blocks
+  float m_lane = -INFINITY;             // largest scaled logit this lane saw
   const int t_begin = it.kv_begin / KT;
   const int t_end = (it.kv_end + KT - 1) / KT;
-  // Softmax reference: fixed per row at its first visible tile and never moved within a pass, so the
-  // accumulators are never rescaled.  Later logits may exceed it by up to 2^64 in the exponent,
-  // which fp32 sums and bf16 probabilities hold for any realistic key count and value magnitude.  If
-  // a row ever exceeds that bound, the workgroup redoes its key range once with the exact row max
-  // (tracked during the first pass) as the reference, which no logit can exceed.
-  float m_ref = -INFINITY, m_true = -INFINITY;
-  for (int pass = 0; pass < 2; ++pass) {
-    if (tid == 0) ovf = 0;
-    {
-      int pg_cur[PPT];
-      WAVEPP_MLA_PAGES(t_begin, pg_cur)
-      WAVEPP_MLA_PAGES(t_begin + 1, pg_nxt)
-#pragma unroll
-      for (int rd = 0; rd < NR; ++rd) {
-        WAVEPP_MLA_LOAD(t_begin, pg_cur, rd * ROUND)
-        WAVEPP_MLA_STORE(0, rd * ROUND)
-      }
-    }
-    __syncthreads();
 
+  for (int pass = 0; pass < 2; ++pass) {
+#pragma unroll
+    for (int r2 = 0; r2 < 2; ++r2)
+#pragma unroll
+      for (int db = 0; db < 4; ++db) oacc[r2][db] = f32x16{};
+    l_lane = 0.0f;
+    dma_tile((lds_u8*)lt0, t_begin);
+    __syncthreads();
     for (int tile = t_begin; tile < t_end; ++tile) {
-      const int buf = (tile - t_begin) & 1;
-      const bool has_next = tile + 1 < t_end;
-      if (has_next) WAVEPP_MLA_LOAD(tile + 1, pg_nxt, 0)
-      const int kbase = tile * KT + 32 * kb;
-      // S^T[key][row]: element r holds key kbase + 8*(r/4) + 4*hf + (r%4)
+      // both pointers select on the same condition: the compiler can tell that the DMAs into `nxt`
+      // never touch `cur`, so the reads of `cur` do not wait for them
+      const bool odd = (tile - t_begin) & 1;
+      const lds_u8* cur = odd ? (const lds_u8*)lt1 : (const lds_u8*)lt0;
+      lds_u8* nxt = odd ? (lds_u8*)lt0 : (lds_u8*)lt1;
+      const bool set_ref = pass == 0 && tile == t_begin;
+      // One tile: the next tile's DMA into `nxt`, logits of (kb, rb) from `cur`, probabilities to
+      // LDS, then O for all 64 rows on the wave's value lanes.
+      if (tile + 1 < t_end) dma_tile(nxt, tile + 1);
+      const int kbase = tile * KT;
+      // S^T of (kb, rb): 36 MFMAs; K fragments read four steps ahead, in source order, so the
+      // reads stay in flight behind the MFMAs
       f32x16 sacc = f32x16{};
       {
-        const __bf16* kl = &lt[buf][k_lane];
-#pragma unroll
+        bf16x8 kbuf[4];
+  #pragma unroll
+        for (int i = 0; i < 4; ++i) kbuf[i] = *reinterpret_cast<lds_bf16x8*>(cur + kofs[i]);
+  #pragma unroll
         for (int s = 0; s < DQ / 16; ++s) {
-          const bf16x8 kf = *reinterpret_cast<const bf16x8*>(kl + 16 * s);
+          const bf16x8 kf = kbuf[s & 3];
+          if (s + 4 < DQ / 16)
+            kbuf[s & 3] = *reinterpret_cast<lds_bf16x8*>(cur + kofs[s & 3] + 128 * ((s + 4) >> 2));
+          // the scheduler would otherwise sink each read down to its MFMA (one read in flight)
+          __builtin_amdgcn_sched_barrier(0);
           sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s], sacc, 0, 0, 0);
         }
-        __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
-#pragma unroll
-        for (int i = 0; i < DQ / 16 - 4; ++i) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-        }
-        __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
       }
-      if ((kbase + 31 > blk_min_lim) || (kbase + 32 > it.kv_end)) {
-        // key > limit or key >= kv_end  <=>  (key - kbase - 4 hf) > bound, one compare per element
-        const int bound = min(limit, it.kv_end - 1) - kbase - 4 * hf;
-#pragma unroll
+      // element r holds key kbase + 32 kb + 8 (r / 4) + 4 hf + (r % 4)
+      if ((kbase + 32 * kb + 31 > blk_min_lim) || (kbase + 32 * kb + 32 > it.kv_end)) {
+        const int bound = bound_base - kbase;
+  #pragma unroll
         for (int r = 0; r < 16; ++r)
           if (8 * (r >> 2) + (r & 3) > bound) sacc[r] = -INFINITY;
       }
       float mx = -INFINITY;
-#pragma unroll
+  #pragma unroll
       for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[r]);
-      mx = halves_max(mx);
-      if (hf == 0) xm[kb][rb][col] = mx;
-      if (has_next) {
-        WAVEPP_MLA_STORE(buf ^ 1, 0)
-        WAVEPP_MLA_LOAD(tile + 1, pg_nxt, ROUND)
+      mx *= sl2;
+      m_lane = fmaxf(m_lane, mx);
+      if (set_ref) {
+        // the item's first tile in the first pass (uniform over the workgroup): both key blocks take
+        // the row maximum over the tile's 64 keys as the reference; -inf means the row sees no key of
+        // the item's range (its visible keys are a prefix of the range), so it never needs one
+        const float mrow = halves_max(mx);
+        if (hf == 0) xch[kb][rb][col] = mrow;
+        lds_barrier();
+        m_ref = fmaxf(xch[0][rb][col], xch[1][rb][col]);
       }
-      __syncthreads();
-      // both waves of a row block see the same maxima and make the same decisions
-      mx = fmaxf(xm[0][rb][col], xm[1][rb][col]) * sl2;
-      m_true = fmaxf(m_true, mx);
-      if (m_ref == -INFINITY) m_ref = mx;
-      if (mx > m_ref + 64.0f) ovf = 1;
       const float m_use = (m_ref == -INFINITY) ? 0.0f : m_ref;
-      float ra = 0.0f, rz = 0.0f;
       bf16x8 pb[2];
-#pragma unroll
+  #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const float e = fast_exp2(fmaf(sacc[r], sl2, -m_use));
-        if (r & 1) rz += e; else ra += e;
+        l_lane += e;
         pb[r >> 3][r & 7] = static_cast<__bf16>(e);
       }
-      l_part += halves_sum(ra + rz);
-      pl[rb][2 * kb][lane] = pb[0];
-      pl[rb][2 * kb + 1][lane] = pb[1];
-      if constexpr (NR == 3) {
-        if (has_next) {
-          WAVEPP_MLA_STORE(buf ^ 1, ROUND)
-          WAVEPP_MLA_LOAD(tile + 1, pg_nxt, 2 * ROUND)
-        }
-      }
-      __syncthreads();
-
-      // O^T[d][row] += V^T[d][key] P^T[key][row] on the wave's value lanes, for all 64 rows
+      pbuf[rb][2 * kb][lane] = pb[0];
+      pbuf[rb][2 * kb + 1][lane] = pb[1];
+      lds_barrier();
+      // O^T[d][row] += V^T[d][key] P^T[key][row]; step t covers keys 16t + 8 (e / 4) + 4 hf + (e % 4).
+      // The fragments of step t + 1 are read while the MFMAs of step t run (source order).
       {
-        const __bf16* vl = &lt[buf][v_lane];
-        // software-pipelined: the V fragment of step n+1 is read while the MFMA pair of step n runs
-        bf16x4 lo = lds_read_tr(vl);
-        bf16x4 hi = lds_read_tr(vl + 8 * STR);
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
-          const bf16x8 p0 = pl[0][ks][lane];
-          const bf16x8 p1 = pl[1][ks][lane];
-#pragma unroll
-          for (int db = 0; db < DW / 32; ++db) {
-            const bf16x8 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-            const int n = ks * (DW / 32) + db + 1;
-            if (n < 4 * (DW / 32)) {
-              const int nks = n / (DW / 32), ndb = n % (DW / 32);
-              lo = lds_read_tr(vl + 16 * nks * STR + 32 * ndb);
-              hi = lds_read_tr(vl + (16 * nks + 8) * STR + 32 * ndb);
-            }
-            oacc[0][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, p0, oacc[0][db], 0, 0, 0);
-            oacc[1][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, p1, oacc[1][db], 0, 0, 0);
+        auto vfrag = [&](int t, int db) {
+          const int o = ((db & 1) ? vb : va) + 128 * (db >> 1) + 18432 * t;
+          const bf16x4 lo = __builtin_bit_cast(bf16x4, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(cur + o)));
+          const bf16x4 hi = __builtin_bit_cast(bf16x4, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(cur + o + dhi)));
+          return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        };
+        bf16x8 p0 = pbuf[0][0][lane], p1 = pbuf[1][0][lane];
+        bf16x8 va4[4];
+  #pragma unroll
+        for (int db = 0; db < 4; ++db) va4[db] = vfrag(0, db);
+  #pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const bf16x8 c0 = p0, c1 = p1;
+          bf16x8 cv[4];
+  #pragma unroll
+          for (int db = 0; db < 4; ++db) cv[db] = va4[db];
+          if (t + 1 < 4) {
+            p0 = pbuf[0][t + 1][lane];
+            p1 = pbuf[1][t + 1][lane];
+  #pragma unroll
+            for (int db = 0; db < 4; ++db) va4[db] = vfrag(t + 1, db);
+          }
+          __builtin_amdgcn_sched_barrier(0);
+  #pragma unroll
+          for (int db = 0; db < 4; ++db) {
+            oacc[0][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cv[db], c0, oacc[0][db], 0, 0, 0);
+            oacc[1][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cv[db], c1, oacc[1][db], 0, 0, 0);
           }
         }
       }
-      if (has_next) {
-        WAVEPP_MLA_STORE(buf ^ 1, (NR - 1) * ROUND)
-        WAVEPP_MLA_PAGES(tile + 2, pg_nxt)
-      }
-      __syncthreads();
+      __syncthreads();   // the next tile's DMA has landed; this tile's reads are done
     }
-    if (pass == 1 || ovf == 0) break;
-    // a reference was exceeded: start over with the exact row max
+    // A reference exceeded by more than 2^64 (log2 units): redo the range with the exact maxima.
+    const float m_half = halves_max(m_lane);
+    if (hf == 0) xch[kb][rb][col] = m_half;
     __syncthreads();
-    m_ref = m_true;
-    l_part = 0.0f;
-#pragma unroll
-    for (int r2 = 0; r2 < 2; ++r2)
-#pragma unroll
-      for (int db = 0; db < DW / 32; ++db) oacc[r2][db] = f32x16{};
+    const float m_row = fmaxf(xch[0][rb][col], xch[1][rb][col]);
+    const bool exceeded = (m_ref != -INFINITY) && (m_row > m_ref + 64.0f);
+    const int any = __syncthreads_or(exceeded ? 1 : 0);
+    if (pass == 1 || !any) break;
+    m_ref = m_row;
+    m_lane = -INFINITY;
   }
-#undef WAVEPP_MLA_PAGES
-#undef WAVEPP_MLA_LOAD
-#undef WAVEPP_MLA_STORE
 
-  // ---- epilogue: row sum = both key halves; every wave normalizes its value lanes of all 64 rows ----
-  if (hf == 0) xm[kb][rb][col] = l_part;
+  // ---- epilogue: row sums of both key blocks through LDS; every wave normalizes its value lanes
+  // of all 64 rows ---------------------------------------------------------------------------------
+  const float l_half = halves_sum(l_lane);
   __syncthreads();
-  if (kb == 0 && row_ok && hf == 0) {
-    const float l = xm[0][rb][col] + xm[1][rb][col];
+  if (hf == 0) xch[kb][rb][col] = l_half;
+  __syncthreads();
+  if (kb == 0 && hf == 0 && row_ok) {
+    const float l = xch[0][rb][col] + xch[1][rb][col];
     const float m_use = (m_ref == -INFINITY) ? 0.0f : m_ref;
     const float lse_v = l > 0.0f ? (m_use + __log2f(l)) * kLn2 : -INFINITY;
     if (it.part < 0) {
-      if (lse_out) lse_out[int64_t(rm.cu + tok) * Hq + head] = lse_v;
+      if (lse_out) lse_out[int64_t(rm.cu + tok) * Hq + (prow - tok * G)] = lse_v;
     } else {
       p.lpart[it.part + lrow] = lse_v;
     }
@@ -628,15 +691,15 @@ __global__ __launch_bounds__(256, 1) void attn_mla_kernel(DevPlan p, const __bf1
   for (int r2 = 0; r2 < 2; ++r2) {
     const int r_local = 32 * r2 + col;
     if (r_local >= it.rows) continue;
-    const float l = xm[0][r2][col] + xm[1][r2][col];
+    const float l = xch[0][r2][col] + xch[1][r2][col];
     const float inv_l = l > 0.0f ? 1.0f / l : 0.0f;
     const int pr = it.row0 + r_local;
     const int tk = pr / G;
     const int hd = pr - tk * G;
     if (it.part < 0) {
-      __bf16* orow = out + (int64_t(rm.cu + tk) * Hq + hd) * DV + DW * wave;
+      __bf16* orow = out + (int64_t(rm.cu + tk) * Hq + hd) * DV + 128 * wave;
 #pragma unroll
-      for (int db = 0; db < DW / 32; ++db)
+      for (int db = 0; db < 4; ++db)
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
           bf16x4 v;
@@ -645,9 +708,9 @@ __global__ __launch_bounds__(256, 1) void attn_mla_kernel(DevPlan p, const __bf1
           *reinterpret_cast<bf16x4*>(orow + 32 * db + 8 * u + 4 * hf) = v;
         }
     } else {
-      float* orow = p.opart + int64_t(it.part + r_local) * DV + DW * wave;
+      float* orow = p.opart + int64_t(it.part + r_local) * DV + 128 * wave;
 #pragma unroll
-      for (int db = 0; db < DW / 32; ++db)
+      for (int db = 0; db < 4; ++db)
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
           f32x4 v;

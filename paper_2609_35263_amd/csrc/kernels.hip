@@ -29,6 +29,7 @@
 
 #include <algorithm>
 #include <mutex>
+#include <type_traits>
 
 namespace wavepp {
 
@@ -402,12 +403,15 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_gqa_kernel(DevP
 //     accumulates O for all 64 rows on value lanes [128w, 128w + 128), so each transposed V
 //     fragment read from LDS feeds two MFMAs.
 //   * The next latent tile is copied global -> LDS by the DMA path (global_load_lds, 16 bytes per
-//     lane), issued at the start of a tile into the other of two buffers; no registers stage it.
+//     lane) into the other of two buffers; no registers stage it.  Its 18 instructions per wave go
+//     one after every second logit MFMA: issued back to back they fill the vector-memory queue and
+//     stall the wave for longer than the MFMAs they would otherwise overlap.
 //     The two buffers are distinct LDS objects, and the current and next buffer pointers select
 //     between them on the same condition, so the compiler can tell that the DMAs never touch the
-//     buffer being read: reads of the current buffer do not wait for the DMAs in flight.  The barrier between the probability writes and
+//     buffer being read: the logit reads of the current buffer do not wait for the DMAs in flight
+//     (the P.V reads are inline assembly, below).  The barrier between the probability writes and
 //     the P.V reads only orders LDS accesses (the DMAs stay in flight); the barrier at the end of
-//     a tile waits for them.
+//     a tile waits for them.  The page index of the tile after next is loaded a tile ahead.
 //   * Layout of a tile in LDS: 64 rows of 72 16-byte chunks, unpadded; chunk c of row j is stored
 //     at chunk position c ^ swz(j) of that row.  The swizzle puts the 16 rows read together by a
 //     K fragment load, and the 4 rows x 4 chunks read together by a transposed V load, on distinct
@@ -434,6 +438,28 @@ typedef __attribute__((address_space(3))) const bf16x8 lds_bf16x8;
 __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0); vector-memory and export counts left unwaited
   asm volatile("s_barrier" ::: "memory");
+}
+
+// LDS reads of the latent kernel's P.V step, issued as inline assembly.  The compiler cannot tell
+// that a transposed read (ds_read_b64_tr_b16) of the current tile misses the next tile's DMA into
+// the other buffer, so with its own reads it would wait for the whole DMA (vmcnt(0)) before the
+// first P.V fragment.  These reads are invisible to its wait tracking; the loop waits for each
+// group of fragments itself with s_waitcnt lgkmcnt(0), tied to the group's values, after the next
+// group has been issued.  lgkmcnt(0) also covers any scalar load in flight, so the wait is exact.
+template <int OFF>
+__device__ __forceinline__ bf16x8 lds_rd_b128(const lds_u8* p) {
+  bf16x8 r;
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(r) : "v"(p), "i"(OFF) : "memory");
+  return r;
+}
+template <int OFF>
+__device__ __forceinline__ bf16x4 lds_rd_tr(const lds_u8* p) {
+  bf16x4 r;
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(p), "i"(OFF) : "memory");
+  return r;
+}
+__device__ __forceinline__ void lds_wait4(bf16x8& a, bf16x8& b, bf16x8& c, bf16x8& d) {
+  asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a), "+v"(b), "+v"(c), "+v"(d) :: "memory");
 }
 
 template <int PAGE>
@@ -563,6 +589,7 @@ __global__ __launch_bounds__(256, 1) void attn_mla_kernel(DevPlan p, const __bf1
       for (int db = 0; db < 4; ++db) oacc[r2][db] = f32x16{};
     l_lane = 0.0f;
     dma_tile((lds_u8*)lt0, t_begin);
+    int pg_next = (PAGE >= KT) ? bt[min(t_begin + 1, last_block)] : 0;
     __syncthreads();
     for (int tile = t_begin; tile < t_end; ++tile) {
       // both pointers select on the same condition: the compiler can tell that the DMAs into `nxt`
@@ -573,7 +600,12 @@ __global__ __launch_bounds__(256, 1) void attn_mla_kernel(DevPlan p, const __bf1
       const bool set_ref = pass == 0 && tile == t_begin;
       // One tile: the next tile's DMA into `nxt`, logits of (kb, rb) from `cur`, probabilities to
       // LDS, then O for all 64 rows on the wave's value lanes.
-      if (tile + 1 < t_end) dma_tile(nxt, tile + 1);
+      // whole next tiles of 64-token pages: the 18 DMA instructions go one per two logit MFMAs, so
+      // the wave never stalls on a full vector-memory queue; the page index was loaded a tile ahead
+      const bool dma_spread = PAGE >= KT && tile + 2 <= t_end && (tile + 2) * KT <= n_valid;
+      const char* nbase = reinterpret_cast<const char*>(lat + int64_t(pg_next) * page_stride);
+      if (tile + 1 < t_end && !dma_spread) dma_tile(nxt, tile + 1);
+      pg_next = bt[min(tile + 2, last_block)];
       const int kbase = tile * KT;
       // S^T of (kb, rb): 36 MFMAs; K fragments read four steps ahead, in source order, so the
       // reads stay in flight behind the MFMAs
@@ -587,6 +619,12 @@ __global__ __launch_bounds__(256, 1) void attn_mla_kernel(DevPlan p, const __bf1
           const bf16x8 kf = kbuf[s & 3];
           if (s + 4 < DQ / 16)
             kbuf[s & 3] = *reinterpret_cast<lds_bf16x8*>(cur + kofs[s & 3] + 128 * ((s + 4) >> 2));
+          if (dma_spread && (s & 1) == 0) {
+            const int i = s >> 1;
+            const int d = int(dma_d[i / 4] << (24 - 8 * (i % 4))) >> 24;
+            __builtin_amdgcn_global_load_lds(nbase + (dma_o0 + 4096u * i + d), (lds_void*)(nxt + 1024 * (wave_s + 4 * i)),
+                                             16, 0, 0);
+          }
           // the scheduler would otherwise sink each read down to its MFMA (one read in flight)
           __builtin_amdgcn_sched_barrier(0);
           sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s], sacc, 0, 0, 0);
@@ -625,37 +663,50 @@ __global__ __launch_bounds__(256, 1) void attn_mla_kernel(DevPlan p, const __bf1
       pbuf[rb][2 * kb + 1][lane] = pb[1];
       lds_barrier();
       // O^T[d][row] += V^T[d][key] P^T[key][row]; step t covers keys 16t + 8 (e / 4) + 4 hf + (e % 4).
-      // The fragments of step t + 1 are read while the MFMAs of step t run (source order).
+      // Step t + 1's fragments (two probability fragments, four transposed V fragments) are read
+      // while the eight MFMAs of step t run.
       {
-        auto vfrag = [&](int t, int db) {
-          const int o = ((db & 1) ? vb : va) + 128 * (db >> 1) + 18432 * t;
-          const bf16x4 lo = __builtin_bit_cast(bf16x4, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(cur + o)));
-          const bf16x4 hi = __builtin_bit_cast(bf16x4, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(cur + o + dhi)));
-          return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        const lds_u8* pp0 = (const lds_u8*)(&pbuf[0][0][lane]);
+        const lds_u8* pva = cur + va;
+        const lds_u8* pvb = cur + vb;
+        const lds_u8* pha = cur + va + dhi;
+        const lds_u8* phb = cur + vb + dhi;
+        bf16x8 pa[2], pn[2], va4[4], vn4[4];
+        auto issue = [&](auto T, bf16x8 (&pd)[2], bf16x8 (&vd)[4]) {
+          constexpr int t = decltype(T)::value;
+          pd[0] = lds_rd_b128<1024 * t>(pp0);
+          pd[1] = lds_rd_b128<4096 + 1024 * t>(pp0);
+          constexpr int o = 18432 * t;
+          vd[0] = __builtin_shufflevector(lds_rd_tr<o>(pva), lds_rd_tr<o>(pha), 0, 1, 2, 3, 4, 5, 6, 7);
+          vd[1] = __builtin_shufflevector(lds_rd_tr<o>(pvb), lds_rd_tr<o>(phb), 0, 1, 2, 3, 4, 5, 6, 7);
+          vd[2] = __builtin_shufflevector(lds_rd_tr<o + 128>(pva), lds_rd_tr<o + 128>(pha), 0, 1, 2, 3, 4, 5, 6, 7);
+          vd[3] = __builtin_shufflevector(lds_rd_tr<o + 128>(pvb), lds_rd_tr<o + 128>(phb), 0, 1, 2, 3, 4, 5, 6, 7);
         };
-        bf16x8 p0 = pbuf[0][0][lane], p1 = pbuf[1][0][lane];
-        bf16x8 va4[4];
-  #pragma unroll
-        for (int db = 0; db < 4; ++db) va4[db] = vfrag(0, db);
-  #pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          const bf16x8 c0 = p0, c1 = p1;
-          bf16x8 cv[4];
-  #pragma unroll
-          for (int db = 0; db < 4; ++db) cv[db] = va4[db];
-          if (t + 1 < 4) {
-            p0 = pbuf[0][t + 1][lane];
-            p1 = pbuf[1][t + 1][lane];
-  #pragma unroll
-            for (int db = 0; db < 4; ++db) va4[db] = vfrag(t + 1, db);
+        auto wait = [&](bf16x8 (&pd)[2], bf16x8 (&vd)[4]) {
+          lds_wait4(vd[0], vd[1], vd[2], vd[3]);
+          asm volatile("" : "+v"(pd[0]), "+v"(pd[1]));
+        };
+        issue(std::integral_constant<int, 0>{}, pa, va4);
+        wait(pa, va4);
+        auto step = [&](auto T) {
+          constexpr int t = decltype(T)::value;
+          if constexpr (t + 1 < 4) issue(std::integral_constant<int, t + 1>{}, pn, vn4);
+          __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+          for (int db = 0; db < 4; ++db) {
+            oacc[0][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va4[db], pa[0], oacc[0][db], 0, 0, 0);
+            oacc[1][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va4[db], pa[1], oacc[1][db], 0, 0, 0);
           }
           __builtin_amdgcn_sched_barrier(0);
-  #pragma unroll
-          for (int db = 0; db < 4; ++db) {
-            oacc[0][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cv[db], c0, oacc[0][db], 0, 0, 0);
-            oacc[1][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cv[db], c1, oacc[1][db], 0, 0, 0);
+          if constexpr (t + 1 < 4) {
+            wait(pn, vn4);
+            pa[0] = pn[0]; pa[1] = pn[1];
+#pragma unroll
+            for (int db = 0; db < 4; ++db) va4[db] = vn4[db];
           }
-        }
+        };
+        step(std::integral_constant<int, 0>{}); step(std::integral_constant<int, 1>{});
+        step(std::integral_constant<int, 2>{}); step(std::integral_constant<int, 3>{});
       }
       __syncthreads();   // the next tile's DMA has landed; this tile's reads are done
     }

@@ -14,6 +14,10 @@ hipError_t launch_attention(const DevPlan&, const void*, const void*, const void
 }
 hipError_t launch_merge(const DevPlan&, void*, float*, hipStream_t) { return hipErrorNotSupported; }
 hipError_t launch_upload(const void*, void*, size_t, hipStream_t) { return hipErrorNotSupported; }
+hipError_t noalloc_scratch(void** ptr) {
+  *ptr = nullptr;
+  return hipErrorNotSupported;
+}
 hipError_t launch_kda_prefill(const KdaDevPlan&, const void*, const void*, const void*, const float*, const float*,
                               float*, void*, hipStream_t) {
   return hipErrorNotSupported;

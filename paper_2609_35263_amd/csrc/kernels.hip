@@ -461,6 +461,11 @@ __device__ __forceinline__ bf16x4 lds_rd_tr(const lds_u8* p) {
 __device__ __forceinline__ void lds_wait4(bf16x8& a, bf16x8& b, bf16x8& c, bf16x8& d) {
   asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a), "+v"(b), "+v"(c), "+v"(d) :: "memory");
 }
+__device__ __forceinline__ void lds_wait_tr8(bf16x4 (&f)[8]) {
+  asm volatile("s_waitcnt lgkmcnt(0)"
+               : "+v"(f[0]), "+v"(f[1]), "+v"(f[2]), "+v"(f[3]), "+v"(f[4]), "+v"(f[5]), "+v"(f[6]), "+v"(f[7])
+               :: "memory");
+}
 
 template <int PAGE>
 __global__ __launch_bounds__(256, 1) void attn_mla_kernel(DevPlan p, const __bf16* __restrict__ q,
@@ -630,6 +635,25 @@ __global__ __launch_bounds__(256, 1) void attn_mla_kernel(DevPlan p, const __bf1
           sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s], sacc, 0, 0, 0);
         }
       }
+      // the first P.V step's transposed V fragments do not depend on the probabilities: read them now,
+      // so that they land during the softmax
+      const lds_u8* pva = cur + va;
+      const lds_u8* pvb = cur + vb;
+      const lds_u8* pha = cur + va + dhi;
+      const lds_u8* phb = cur + vb + dhi;
+      bf16x4 vraw[8];
+      auto issue_v = [&](auto T, bf16x4 (&vr)[8]) {
+        constexpr int o = 18432 * decltype(T)::value;
+        vr[0] = lds_rd_tr<o>(pva);
+        vr[1] = lds_rd_tr<o>(pha);
+        vr[2] = lds_rd_tr<o>(pvb);
+        vr[3] = lds_rd_tr<o>(phb);
+        vr[4] = lds_rd_tr<o + 128>(pva);
+        vr[5] = lds_rd_tr<o + 128>(pha);
+        vr[6] = lds_rd_tr<o + 128>(pvb);
+        vr[7] = lds_rd_tr<o + 128>(phb);
+      };
+      issue_v(std::integral_constant<int, 0>{}, vraw);
       // element r holds key kbase + 32 kb + 8 (r / 4) + 4 hf + (r % 4)
       if ((kbase + 32 * kb + 31 > blk_min_lim) || (kbase + 32 * kb + 32 > it.kv_end)) {
         const int bound = bound_base - kbase;
@@ -663,34 +687,31 @@ __global__ __launch_bounds__(256, 1) void attn_mla_kernel(DevPlan p, const __bf1
       pbuf[rb][2 * kb + 1][lane] = pb[1];
       lds_barrier();
       // O^T[d][row] += V^T[d][key] P^T[key][row]; step t covers keys 16t + 8 (e / 4) + 4 hf + (e % 4).
-      // Step t + 1's fragments (two probability fragments, four transposed V fragments) are read
-      // while the eight MFMAs of step t run.
+      // Step t + 1's fragments (two probability fragments, eight transposed V halves) are read while
+      // the eight MFMAs of step t run; a fragment's halves are joined only after the wait for them.
       {
         const lds_u8* pp0 = (const lds_u8*)(&pbuf[0][0][lane]);
-        const lds_u8* pva = cur + va;
-        const lds_u8* pvb = cur + vb;
-        const lds_u8* pha = cur + va + dhi;
-        const lds_u8* phb = cur + vb + dhi;
-        bf16x8 pa[2], pn[2], va4[4], vn4[4];
-        auto issue = [&](auto T, bf16x8 (&pd)[2], bf16x8 (&vd)[4]) {
+        auto issue_p = [&](auto T, bf16x8 (&pd)[2]) {
           constexpr int t = decltype(T)::value;
           pd[0] = lds_rd_b128<1024 * t>(pp0);
           pd[1] = lds_rd_b128<4096 + 1024 * t>(pp0);
-          constexpr int o = 18432 * t;
-          vd[0] = __builtin_shufflevector(lds_rd_tr<o>(pva), lds_rd_tr<o>(pha), 0, 1, 2, 3, 4, 5, 6, 7);
-          vd[1] = __builtin_shufflevector(lds_rd_tr<o>(pvb), lds_rd_tr<o>(phb), 0, 1, 2, 3, 4, 5, 6, 7);
-          vd[2] = __builtin_shufflevector(lds_rd_tr<o + 128>(pva), lds_rd_tr<o + 128>(pha), 0, 1, 2, 3, 4, 5, 6, 7);
-          vd[3] = __builtin_shufflevector(lds_rd_tr<o + 128>(pvb), lds_rd_tr<o + 128>(phb), 0, 1, 2, 3, 4, 5, 6, 7);
         };
-        auto wait = [&](bf16x8 (&pd)[2], bf16x8 (&vd)[4]) {
-          lds_wait4(vd[0], vd[1], vd[2], vd[3]);
-          asm volatile("" : "+v"(pd[0]), "+v"(pd[1]));
+        auto join = [&](bf16x4 (&vr)[8], bf16x8 (&vd)[4]) {
+#pragma unroll
+          for (int db = 0; db < 4; ++db) vd[db] = __builtin_shufflevector(vr[2 * db], vr[2 * db + 1], 0, 1, 2, 3, 4, 5, 6, 7);
         };
-        issue(std::integral_constant<int, 0>{}, pa, va4);
-        wait(pa, va4);
+        bf16x8 pa[2], pn[2], va4[4];
+        bf16x4 vn[8];
+        issue_p(std::integral_constant<int, 0>{}, pa);
+        lds_wait_tr8(vraw);   // (landed before the barrier: this ties the values to the wait)
+        asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(pa[0]), "+v"(pa[1]) :: "memory");
+        join(vraw, va4);
         auto step = [&](auto T) {
           constexpr int t = decltype(T)::value;
-          if constexpr (t + 1 < 4) issue(std::integral_constant<int, t + 1>{}, pn, vn4);
+          if constexpr (t + 1 < 4) {
+            issue_p(std::integral_constant<int, t + 1>{}, pn);
+            issue_v(std::integral_constant<int, t + 1>{}, vn);
+          }
           __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
           for (int db = 0; db < 4; ++db) {
@@ -699,10 +720,10 @@ __global__ __launch_bounds__(256, 1) void attn_mla_kernel(DevPlan p, const __bf1
           }
           __builtin_amdgcn_sched_barrier(0);
           if constexpr (t + 1 < 4) {
-            wait(pn, vn4);
+            lds_wait_tr8(vn);
+            asm volatile("" : "+v"(pn[0]), "+v"(pn[1]));
             pa[0] = pn[0]; pa[1] = pn[1];
-#pragma unroll
-            for (int db = 0; db < 4; ++db) va4[db] = vn4[db];
+            join(vn, va4);
           }
         };
         step(std::integral_constant<int, 0>{}); step(std::integral_constant<int, 1>{});

@@ -450,7 +450,11 @@ int wavepp_attn_plan(const wavepp_attn_shape* shape, const wavepp_batch* batch, 
   }
   // key-range splits: forced by max_splits, or chosen so that a small wave still fills the chip,
   // each automatic split keeping at least 1,024 keys (grouped kernel) or 512 (latent kernel)
-  const int64_t fill_target = 1024;  // resident workgroups the chip can hold, x2
+  // Split a wave with fewer base items than this until it has about that many.  512 items are two
+  // workgroups per CU of the 4-wave form, or two rounds of the one-per-CU forms; on the short-chunk
+  // waves (c = 16 .. 128) it gave the fastest or within 0.5 % of the fastest split count, against
+  // 1,024 items, which cost 2-11 % in the extra partials and merge work.
+  const int64_t fill_target = 512;
   const int64_t min_split_tiles = (mla ? 512 : 1024) / KT;
   std::vector<WorkItem> items;
   int64_t part_rows = 0;
@@ -460,7 +464,7 @@ int wavepp_attn_plan(const wavepp_attn_shape* shape, const wavepp_batch* batch, 
     int64_t S = 1;
     if (max_splits >= 1) {
       S = std::min<int64_t>(max_splits, ntiles);
-    } else if (int64_t(base.size()) < fill_target / 2) {
+    } else if (int64_t(base.size()) < fill_target) {
       S = std::min<int64_t>(ceil_div(fill_target, int64_t(base.size())), ntiles / min_split_tiles);
       S = std::max<int64_t>(S, 1);
     }

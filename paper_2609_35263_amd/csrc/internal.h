@@ -11,7 +11,7 @@ constexpr uint32_t kMagic = 0x57415650u;   // "WAVP"
 constexpr int kGqaRowsPerItem = 256;       // grouped kernel: 8 waves x 32 query rows
 constexpr int kKvTile = 128;               // grouped kernel: keys per inner-loop tile
 constexpr int kNumXcd = 8;                 // L2 domains a launch is spread over, round-robin
-constexpr int kMlaRowsPerItem = 64;        // latent kernel: query rows per work item
+constexpr int kMlaRowsPerItem = 128;       // latent kernel: query rows per work item
 constexpr int kMlaKvTile = 64;             // latent kernel: keys per tile
 
 // Header at the start of the uploaded metadata.

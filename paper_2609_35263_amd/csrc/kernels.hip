@@ -391,27 +391,32 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_gqa_kernel(DevP
 // Latent attention in absorbed form: every query head attends over one shared 576-wide latent per
 // token (keys = the whole latent, values = its first 512 lanes).  Page size PAGE (16 or 64).
 //
-// One workgroup = 4 waves (one per SIMD) = 64 query rows; latent tiles of 64 keys.
-//   * Logits: wave w computes S^T for key block w / 2 (32 keys) and row block w % 2 (32 rows), 36
-//     MFMAs with its 32 Q rows in registers.
-//   * Softmax reference: fixed per row at the item's first tile (both waves of a row block take
-//     the maximum over the tile's 64 keys, exchanged once through LDS) and never moved, so the
-//     accumulators are never rescaled and no maximum is exchanged afterwards.  If a later logit
-//     exceeds the reference by more than 2^64 the workgroup redoes its key range with the exact
-//     row maxima (tracked per lane, combined at the end).
+// One workgroup = 4 waves (one per SIMD) = 128 query rows; latent tiles of 64 keys.  Each staged
+// 72 KiB tile serves 128 rows, so the L2 -> LDS traffic per FLOP is half that of 64-row items.
+//   * Logits: wave w computes S^T for its own 32 rows (row block w) against both 32-key blocks of
+//     the tile: 2 x 36 MFMAs sharing each Q fragment, with its 32 Q rows in registers.  The P.V
+//     accumulators take all 256 AGPRs, so the logit MFMAs are inline assembly with VGPR
+//     accumulators (mfma_v_pair).
+//   * Softmax reference: fixed per row at the item's first tile (the row's two lanes hold its
+//     maximum over the tile's 64 keys between them) and never moved, so the accumulators are never
+//     rescaled.  If a later logit exceeds the reference by more than 2^64 the workgroup redoes its
+//     key range with the exact row maxima (tracked per lane, combined at the end).
 //   * Values: the bf16 probabilities, already in MFMA B-operand order, go through LDS; wave w
-//     accumulates O for all 64 rows on value lanes [128w, 128w + 128), so each transposed V
-//     fragment read from LDS feeds two MFMAs.
+//     accumulates O for all 128 rows on value lanes [128w, 128w + 128), so each transposed V
+//     fragment read from LDS feeds four MFMAs.
 //   * The next latent tile is copied global -> LDS by the DMA path (global_load_lds, 16 bytes per
 //     lane) into the other of two buffers; no registers stage it.  Its 18 instructions per wave go
-//     one after every second logit MFMA: issued back to back they fill the vector-memory queue and
-//     stall the wave for longer than the MFMAs they would otherwise overlap.
+//     one after every fourth logit MFMA: issued back to back they fill the vector-memory queue and
+//     stall the wave for longer than the MFMAs they would otherwise overlap.  Each instruction's
+//     source is a scalar page base plus a 32-bit lane offset rebuilt next to its use.
 //     The two buffers are distinct LDS objects, and the current and next buffer pointers select
 //     between them on the same condition, so the compiler can tell that the DMAs never touch the
 //     buffer being read: the logit reads of the current buffer do not wait for the DMAs in flight
 //     (the P.V reads are inline assembly, below).  The barrier between the probability writes and
 //     the P.V reads only orders LDS accesses (the DMAs stay in flight); the barrier at the end of
 //     a tile waits for them.  The page index of the tile after next is loaded a tile ahead.
+//   * LDS: two 72 KiB tile buffers and 16 KiB of probabilities, the whole 160 KiB; after a pass the
+//     probability buffer also carries the waves' overflow flags and the row sums.
 //   * Layout of a tile in LDS: 64 rows of 72 16-byte chunks, unpadded; chunk c of row j is stored
 //     at chunk position c ^ swz(j) of that row.  The swizzle puts the 16 rows read together by a
 //     K fragment load, and the 4 rows x 4 chunks read together by a transposed V load, on distinct
@@ -424,7 +429,8 @@ constexpr int ROW_BYTES = DQ * 2;            // 1152
 constexpr int TILE_BYTES = KT * ROW_BYTES;   // 73728
 constexpr int NDMA = KT * CPR / 64 / 4;      // DMA instructions (64 lanes x 16 bytes) per wave per tile: 18
 static_assert(NDMA * 4 * 64 == KT * CPR, "tile covered exactly by the DMA instructions");
-static_assert(kMlaRowsPerItem == 64 && kMlaKvTile == KT, "planner and kernel agree");
+constexpr int RPI = kMlaRowsPerItem;         // query rows per work item (32 per wave)
+static_assert(RPI == 128 && kMlaKvTile == KT, "planner and kernel agree");
 // chunk position of logical chunk c of row j: c ^ swz(j) (swz < 8 keeps it in c's aligned group of 8)
 __device__ __forceinline__ uint32_t swz(uint32_t j) { return (((j >> 1) & 1u) << 2) | ((j >> 2) & 3u); }
 }  // namespace mla
@@ -467,16 +473,41 @@ __device__ __forceinline__ void lds_wait_tr8(bf16x4 (&f)[8]) {
                :: "memory");
 }
 
+
+// Logit MFMAs of the latent kernel, as inline assembly with their accumulators in VGPRs.  The P.V
+// accumulators of the 128-row form fill all 256 AGPRs, and the compiler gives every MFMA of a
+// function that uses AGPRs the AGPR form, so with the builtin the logit accumulators would push O
+// out of its registers.  Hazards the compiler cannot see here are covered explicitly: two wait
+// states before each pair (a VALU write of an operand), none between pairs of one chain (each
+// accumulates into exactly its own registers), and 24 after the last pair before any other
+// instruction reads or writes the results (mfma_v_drain).
+__device__ __forceinline__ void mfma_v_pair0(f32x16& a0, f32x16& a1, const bf16x8& k0, const bf16x8& k1,
+                                             const bf16x8& qv) {
+  asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %2, %4, 0\n\tv_mfma_f32_32x32x16_bf16 %1, %3, %4, 0"
+               : "=&v"(a0), "=&v"(a1) : "v"(k0), "v"(k1), "v"(qv));
+}
+__device__ __forceinline__ void mfma_v_pair(f32x16& a0, f32x16& a1, const bf16x8& k0, const bf16x8& k1,
+                                            const bf16x8& qv) {
+  asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %2, %4, %0\n\tv_mfma_f32_32x32x16_bf16 %1, %3, %4, %1"
+               : "+v"(a0), "+v"(a1) : "v"(k0), "v"(k1), "v"(qv));
+}
+__device__ __forceinline__ void mfma_v_drain(f32x16& a0, f32x16& a1) {
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" : "+v"(a0), "+v"(a1));
+}
+
 template <int PAGE>
 __global__ __launch_bounds__(256, 1) void attn_mla_kernel(DevPlan p, const __bf16* __restrict__ q,
                                                           const __bf16* __restrict__ lat, __bf16* __restrict__ out,
                                                           float* __restrict__ lse_out) {
   using namespace mla;
   constexpr int PPT = (PAGE >= KT) ? 1 : KT / PAGE;   // pages per tile
+  constexpr int NRB = RPI / 32;                       // row blocks (one per wave)
   __shared__ __attribute__((aligned(1024))) unsigned char lt0[TILE_BYTES];
   __shared__ __attribute__((aligned(1024))) unsigned char lt1[TILE_BYTES];
-  __shared__ __attribute__((aligned(16))) bf16x8 pbuf[2][4][64];   // [row block][16-key step][lane]
-  __shared__ float xch[2][2][32];                                  // [key block][row block][row]
+  // probabilities [row block][16-key step][lane]; after a pass the same bytes carry the workgroup's
+  // flags and row sums
+  __shared__ __attribute__((aligned(16))) bf16x8 pbuf[NRB][4][64];
+  float* const xf = reinterpret_cast<float*>(&pbuf[0][0][0]);
 
   if (!meta_ok(p)) return;
   const WorkItem it = p.items[blockIdx.x];
@@ -485,7 +516,7 @@ __global__ __launch_bounds__(256, 1) void attn_mla_kernel(DevPlan p, const __bf1
   const int Hq = p.num_q_heads;
   const int G = Hq;                     // a single latent head
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, col = lane & 31, hf = lane >> 5;
-  const int kb = wave >> 1, rb = wave & 1;
+  const int rb = wave;
   const int n_valid = rm.prefix + rm.chunk;
   const int32_t* __restrict__ bt = p.bt + rm.bt_row;
   const int64_t page_stride = int64_t(PAGE) * DQ;
@@ -505,15 +536,14 @@ __global__ __launch_bounds__(256, 1) void attn_mla_kernel(DevPlan p, const __bf1
   // smallest limit among the row block's lanes (lanes past it.rows use row 0's limit)
   const int blk_min_lim = rm.prefix + (it.row0 + ((rb * 32 + 32 <= it.rows) ? rb * 32 : 0)) / G;
   const float sl2 = p.softmax_scale * kLog2e;
-  const int bound_base = min(limit, it.kv_end - 1) - 32 * kb - 4 * hf;
+  const int bound_base = min(limit, it.kv_end - 1) - 4 * hf;
 
   // ---- per-lane LDS byte offsets ---------------------------------------------------------------
-  // K fragment of step s = 4a + b: row 32kb + col, chunk 2s + hf -> kofs[b] + 128a
-  // (the swizzle has period 16 in the row)
+  // K fragment of key block kb, step s = 4a + b: row 32kb + col, chunk 2s + hf
+  //   -> kofs[b] + 36864 kb + 128a (the swizzle has period 16 in the row)
   int kofs[4];
 #pragma unroll
-  for (int b = 0; b < 4; ++b)
-    kofs[b] = (32 * kb + col) * ROW_BYTES + 16 * int((2u * b + hf) ^ swz(uint32_t(col)));
+  for (int b = 0; b < 4; ++b) kofs[b] = col * ROW_BYTES + 16 * int((2u * b + hf) ^ swz(uint32_t(col)));
   // transposed V fragment of step t (16 keys), value block db (32 lanes of d), half lo/hi:
   //   rows 16t + 4hf + (lane & 15) / 4 (+8 for hi), d = 128 wave + 32 db + 16 g + 4 (lane & 3)
   //   -> (db even ? va : vb) + 128 (db >> 1) + 18432 t (+ dhi for hi)
@@ -553,7 +583,8 @@ __global__ __launch_bounds__(256, 1) void attn_mla_kernel(DevPlan p, const __bf1
   auto dma_tile = [&](lds_u8* buf, int tile) {
     const int kbase = tile * KT;
     if (PAGE >= KT && kbase + KT <= n_valid) {
-      const char* tbase = reinterpret_cast<const char*>(lat + int64_t(bt[tile]) * page_stride);
+      const int pg = __builtin_amdgcn_readfirstlane(bt[tile]);
+      const char* tbase = reinterpret_cast<const char*>(lat + int64_t(pg) * page_stride);
 #pragma unroll
       for (int i = 0; i < NDMA; ++i) {
         const int d = int(dma_d[i / 4] << (24 - 8 * (i % 4))) >> 24;
@@ -580,21 +611,21 @@ __global__ __launch_bounds__(256, 1) void attn_mla_kernel(DevPlan p, const __bf1
     }
   };
 
-  f32x16 oacc[2][4];                    // [row block][value block]: O^T for value lanes 128 wave + 32 db
-  float l_lane = 0.0f;                  // this lane's part of its row's sum (its key block, its half)
-  float m_ref = -INFINITY;              // row reference (log2 units, scaled), equal in both key blocks
+  f32x16 oacc[NRB][4];                  // [row block][value block]: O^T for value lanes 128 wave + 32 db
+  float l_lane = 0.0f;                  // this lane's part of its row's sum (its half of every tile)
+  float m_ref = -INFINITY;              // row reference (log2 units, scaled)
   float m_lane = -INFINITY;             // largest scaled logit this lane saw
   const int t_begin = it.kv_begin / KT;
   const int t_end = (it.kv_end + KT - 1) / KT;
 
   for (int pass = 0; pass < 2; ++pass) {
 #pragma unroll
-    for (int r2 = 0; r2 < 2; ++r2)
+    for (int r2 = 0; r2 < NRB; ++r2)
 #pragma unroll
       for (int db = 0; db < 4; ++db) oacc[r2][db] = f32x16{};
     l_lane = 0.0f;
     dma_tile((lds_u8*)lt0, t_begin);
-    int pg_next = (PAGE >= KT) ? bt[min(t_begin + 1, last_block)] : 0;
+    int pg_next = (PAGE >= KT) ? bt[min(t_begin + 1, last_block)] : 0;   // made scalar at its use, a tile later
     __syncthreads();
     for (int tile = t_begin; tile < t_end; ++tile) {
       // both pointers select on the same condition: the compiler can tell that the DMAs into `nxt`
@@ -603,27 +634,37 @@ __global__ __launch_bounds__(256, 1) void attn_mla_kernel(DevPlan p, const __bf1
       const lds_u8* cur = odd ? (const lds_u8*)lt1 : (const lds_u8*)lt0;
       lds_u8* nxt = odd ? (lds_u8*)lt0 : (lds_u8*)lt1;
       const bool set_ref = pass == 0 && tile == t_begin;
-      // One tile: the next tile's DMA into `nxt`, logits of (kb, rb) from `cur`, probabilities to
-      // LDS, then O for all 64 rows on the wave's value lanes.
-      // whole next tiles of 64-token pages: the 18 DMA instructions go one per two logit MFMAs, so
+      // One tile: the next tile's DMA into `nxt`, logits of the wave's 32 rows against all 64 keys
+      // from `cur`, probabilities to LDS, then O for all rows on the wave's value lanes.
+      // whole next tiles of 64-token pages: the 18 DMA instructions go one per four logit MFMAs, so
       // the wave never stalls on a full vector-memory queue; the page index was loaded a tile ahead
       const bool dma_spread = PAGE >= KT && tile + 2 <= t_end && (tile + 2) * KT <= n_valid;
-      const char* nbase = reinterpret_cast<const char*>(lat + int64_t(pg_next) * page_stride);
+      const char* nbase = reinterpret_cast<const char*>(lat + int64_t(__builtin_amdgcn_readfirstlane(pg_next)) * page_stride);
       if (tile + 1 < t_end && !dma_spread) dma_tile(nxt, tile + 1);
       pg_next = bt[min(tile + 2, last_block)];
+      // the DMA offsets are rebuilt next to each use (two ALU operations) instead of being held in
+      // 18 registers across the loop
+      asm volatile("" : "+v"(dma_d[0]), "+v"(dma_d[1]), "+v"(dma_d[2]), "+v"(dma_d[3]), "+v"(dma_d[4]));
       const int kbase = tile * KT;
-      // S^T of (kb, rb): 36 MFMAs; K fragments read four steps ahead, in source order, so the
-      // reads stay in flight behind the MFMAs
-      f32x16 sacc = f32x16{};
+      // S^T of both key blocks: 2 x 36 MFMAs sharing each Q fragment; K fragments read KPF steps
+      // ahead, in source order, so the reads stay in flight behind the MFMAs
+      f32x16 sacc[2];
       {
-        bf16x8 kbuf[4];
+        constexpr int KPF = 2;
+        bf16x8 kbuf[2][KPF];
   #pragma unroll
-        for (int i = 0; i < 4; ++i) kbuf[i] = *reinterpret_cast<lds_bf16x8*>(cur + kofs[i]);
+        for (int i = 0; i < KPF; ++i) {
+          kbuf[0][i] = *reinterpret_cast<lds_bf16x8*>(cur + kofs[i & 3] + 128 * (i >> 2));
+          kbuf[1][i] = *reinterpret_cast<lds_bf16x8*>(cur + kofs[i & 3] + 128 * (i >> 2) + 32 * ROW_BYTES);
+        }
   #pragma unroll
         for (int s = 0; s < DQ / 16; ++s) {
-          const bf16x8 kf = kbuf[s & 3];
-          if (s + 4 < DQ / 16)
-            kbuf[s & 3] = *reinterpret_cast<lds_bf16x8*>(cur + kofs[s & 3] + 128 * ((s + 4) >> 2));
+          const bf16x8 k0 = kbuf[0][s % KPF], k1 = kbuf[1][s % KPF];
+          if (s + KPF < DQ / 16) {
+            const int n = s + KPF;
+            kbuf[0][s % KPF] = *reinterpret_cast<lds_bf16x8*>(cur + kofs[n & 3] + 128 * (n >> 2));
+            kbuf[1][s % KPF] = *reinterpret_cast<lds_bf16x8*>(cur + kofs[n & 3] + 128 * (n >> 2) + 32 * ROW_BYTES);
+          }
           if (dma_spread && (s & 1) == 0) {
             const int i = s >> 1;
             const int d = int(dma_d[i / 4] << (24 - 8 * (i % 4))) >> 24;
@@ -632,8 +673,10 @@ __global__ __launch_bounds__(256, 1) void attn_mla_kernel(DevPlan p, const __bf1
           }
           // the scheduler would otherwise sink each read down to its MFMA (one read in flight)
           __builtin_amdgcn_sched_barrier(0);
-          sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s], sacc, 0, 0, 0);
+          if (s == 0) mfma_v_pair0(sacc[0], sacc[1], k0, k1, qf[s]);
+          else mfma_v_pair(sacc[0], sacc[1], k0, k1, qf[s]);
         }
+        mfma_v_drain(sacc[0], sacc[1]);
       }
       // the first P.V step's transposed V fragments do not depend on the probabilities: read them now,
       // so that they land during the softmax
@@ -654,57 +697,61 @@ __global__ __launch_bounds__(256, 1) void attn_mla_kernel(DevPlan p, const __bf1
         vr[7] = lds_rd_tr<o + 128>(phb);
       };
       issue_v(std::integral_constant<int, 0>{}, vraw);
-      // element r holds key kbase + 32 kb + 8 (r / 4) + 4 hf + (r % 4)
-      if ((kbase + 32 * kb + 31 > blk_min_lim) || (kbase + 32 * kb + 32 > it.kv_end)) {
-        const int bound = bound_base - kbase;
-  #pragma unroll
-        for (int r = 0; r < 16; ++r)
-          if (8 * (r >> 2) + (r & 3) > bound) sacc[r] = -INFINITY;
-      }
+      // element r of sacc[kb] holds key kbase + 32 kb + 8 (r / 4) + 4 hf + (r % 4)
       float mx = -INFINITY;
   #pragma unroll
-      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[r]);
+      for (int kb = 0; kb < 2; ++kb) {
+        if ((kbase + 32 * kb + 31 > blk_min_lim) || (kbase + 32 * kb + 32 > it.kv_end)) {
+          const int bound = bound_base - kbase - 32 * kb;
+  #pragma unroll
+          for (int r = 0; r < 16; ++r)
+            if (8 * (r >> 2) + (r & 3) > bound) sacc[kb][r] = -INFINITY;
+        }
+  #pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[kb][r]);
+      }
       mx *= sl2;
       m_lane = fmaxf(m_lane, mx);
-      if (set_ref) {
-        // the item's first tile in the first pass (uniform over the workgroup): both key blocks take
-        // the row maximum over the tile's 64 keys as the reference; -inf means the row sees no key of
-        // the item's range (its visible keys are a prefix of the range), so it never needs one
-        const float mrow = halves_max(mx);
-        if (hf == 0) xch[kb][rb][col] = mrow;
-        lds_barrier();
-        m_ref = fmaxf(xch[0][rb][col], xch[1][rb][col]);
-      }
+      // the item's first tile in the first pass (uniform over the workgroup): the reference is the
+      // row maximum over the tile's 64 keys, which the row's two lanes hold between them; -inf means
+      // the row sees no key of the item's range (its visible keys are a prefix of the range), so it
+      // never needs one
+      if (set_ref) m_ref = halves_max(mx);
       const float m_use = (m_ref == -INFINITY) ? 0.0f : m_ref;
-      bf16x8 pb[2];
   #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float e = fast_exp2(fmaf(sacc[r], sl2, -m_use));
-        l_lane += e;
-        pb[r >> 3][r & 7] = static_cast<__bf16>(e);
+      for (int kb = 0; kb < 2; ++kb) {
+        bf16x8 pb[2];
+  #pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float e = fast_exp2(fmaf(sacc[kb][r], sl2, -m_use));
+          l_lane += e;
+          pb[r >> 3][r & 7] = static_cast<__bf16>(e);
+        }
+        pbuf[rb][2 * kb][lane] = pb[0];
+        pbuf[rb][2 * kb + 1][lane] = pb[1];
       }
-      pbuf[rb][2 * kb][lane] = pb[0];
-      pbuf[rb][2 * kb + 1][lane] = pb[1];
       lds_barrier();
       // O^T[d][row] += V^T[d][key] P^T[key][row]; step t covers keys 16t + 8 (e / 4) + 4 hf + (e % 4).
-      // Step t + 1's fragments (two probability fragments, eight transposed V halves) are read while
-      // the eight MFMAs of step t run; a fragment's halves are joined only after the wait for them.
+      // Step t + 1's fragments (four probability fragments, eight transposed V halves) are read while
+      // the sixteen MFMAs of step t run; a fragment's halves are joined only after the wait for them.
       {
         const lds_u8* pp0 = (const lds_u8*)(&pbuf[0][0][lane]);
-        auto issue_p = [&](auto T, bf16x8 (&pd)[2]) {
+        auto issue_p = [&](auto T, bf16x8 (&pd)[NRB]) {
           constexpr int t = decltype(T)::value;
           pd[0] = lds_rd_b128<1024 * t>(pp0);
           pd[1] = lds_rd_b128<4096 + 1024 * t>(pp0);
+          pd[2] = lds_rd_b128<8192 + 1024 * t>(pp0);
+          pd[3] = lds_rd_b128<12288 + 1024 * t>(pp0);
         };
         auto join = [&](bf16x4 (&vr)[8], bf16x8 (&vd)[4]) {
 #pragma unroll
           for (int db = 0; db < 4; ++db) vd[db] = __builtin_shufflevector(vr[2 * db], vr[2 * db + 1], 0, 1, 2, 3, 4, 5, 6, 7);
         };
-        bf16x8 pa[2], pn[2], va4[4];
+        bf16x8 pa[NRB], pn[NRB], va4[4];
         bf16x4 vn[8];
         issue_p(std::integral_constant<int, 0>{}, pa);
         lds_wait_tr8(vraw);   // (landed before the barrier: this ties the values to the wait)
-        asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(pa[0]), "+v"(pa[1]) :: "memory");
+        lds_wait4(pa[0], pa[1], pa[2], pa[3]);
         join(vraw, va4);
         auto step = [&](auto T) {
           constexpr int t = decltype(T)::value;
@@ -714,15 +761,16 @@ __global__ __launch_bounds__(256, 1) void attn_mla_kernel(DevPlan p, const __bf1
           }
           __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-          for (int db = 0; db < 4; ++db) {
-            oacc[0][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va4[db], pa[0], oacc[0][db], 0, 0, 0);
-            oacc[1][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va4[db], pa[1], oacc[1][db], 0, 0, 0);
-          }
+          for (int db = 0; db < 4; ++db)
+#pragma unroll
+            for (int r2 = 0; r2 < NRB; ++r2)
+              oacc[r2][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va4[db], pa[r2], oacc[r2][db], 0, 0, 0);
           __builtin_amdgcn_sched_barrier(0);
           if constexpr (t + 1 < 4) {
             lds_wait_tr8(vn);
-            asm volatile("" : "+v"(pn[0]), "+v"(pn[1]));
-            pa[0] = pn[0]; pa[1] = pn[1];
+            asm volatile("" : "+v"(pn[0]), "+v"(pn[1]), "+v"(pn[2]), "+v"(pn[3]));
+#pragma unroll
+            for (int r2 = 0; r2 < NRB; ++r2) pa[r2] = pn[r2];
             join(vn, va4);
           }
         };
@@ -732,27 +780,29 @@ __global__ __launch_bounds__(256, 1) void attn_mla_kernel(DevPlan p, const __bf1
       __syncthreads();   // the next tile's DMA has landed; this tile's reads are done
     }
     // A reference exceeded by more than 2^64 (log2 units): redo the range with the exact maxima.
-    const float m_half = halves_max(m_lane);
-    if (hf == 0) xch[kb][rb][col] = m_half;
-    __syncthreads();
-    const float m_row = fmaxf(xch[0][rb][col], xch[1][rb][col]);
+    // The row's two lanes hold its maximum between them; the waves' verdicts meet in LDS (the
+    // probability buffer is idle after the loop's last barrier).
+    const float m_row = halves_max(m_lane);
     const bool exceeded = (m_ref != -INFINITY) && (m_row > m_ref + 64.0f);
-    const int any = __syncthreads_or(exceeded ? 1 : 0);
+    const bool wave_any = __builtin_amdgcn_ballot_w64(exceeded) != 0;
+    if (lane == 0) xf[wave] = wave_any ? 1.0f : 0.0f;
+    __syncthreads();
+    bool any = false;
+#pragma unroll
+    for (int w = 0; w < NRB; ++w) any = any || (xf[w] != 0.0f);
+    __syncthreads();   // the flags are read before the next pass writes probabilities
     if (pass == 1 || !any) break;
     m_ref = m_row;
     m_lane = -INFINITY;
   }
 
-  // ---- epilogue: row sums of both key blocks through LDS; every wave normalizes its value lanes
-  // of all 64 rows ---------------------------------------------------------------------------------
-  const float l_half = halves_sum(l_lane);
+  // ---- epilogue: row sums through LDS; every wave normalizes its value lanes of all rows ----------
+  const float l_row = halves_sum(l_lane);
+  if (hf == 0) xf[32 * rb + col] = l_row;
   __syncthreads();
-  if (hf == 0) xch[kb][rb][col] = l_half;
-  __syncthreads();
-  if (kb == 0 && hf == 0 && row_ok) {
-    const float l = xch[0][rb][col] + xch[1][rb][col];
+  if (hf == 0 && row_ok) {
     const float m_use = (m_ref == -INFINITY) ? 0.0f : m_ref;
-    const float lse_v = l > 0.0f ? (m_use + __log2f(l)) * kLn2 : -INFINITY;
+    const float lse_v = l_row > 0.0f ? (m_use + __log2f(l_row)) * kLn2 : -INFINITY;
     if (it.part < 0) {
       if (lse_out) lse_out[int64_t(rm.cu + tok) * Hq + (prow - tok * G)] = lse_v;
     } else {
@@ -760,10 +810,10 @@ __global__ __launch_bounds__(256, 1) void attn_mla_kernel(DevPlan p, const __bf1
     }
   }
 #pragma unroll
-  for (int r2 = 0; r2 < 2; ++r2) {
+  for (int r2 = 0; r2 < NRB; ++r2) {
     const int r_local = 32 * r2 + col;
     if (r_local >= it.rows) continue;
-    const float l = xch[0][r2][col] + xch[1][r2][col];
+    const float l = xf[r_local];
     const float inv_l = l > 0.0f ? 1.0f / l : 0.0f;
     const int pr = it.row0 + r_local;
     const int tk = pr / G;

@@ -198,7 +198,7 @@ def test_latent_plan_shapes():
               softmax_scale=1 / 24, prefix_lens=[100], chunk_lens=[30], block_table=[[1, 4, 0]], kv_shared=True)
     p = wp.plan(**ok)
     info = p.info()
-    assert info["rows_per_item"] == 64 and info["kv_tile"] == 64 and info["num_real_items"] == 30 * 16 // 64 + 1
+    assert info["rows_per_item"] == 128 and info["kv_tile"] == 64 and info["num_real_items"] == 30 * 16 // 128 + 1
     for over, status in [(dict(num_kv_heads=2, num_q_heads=16), -2), (dict(head_dim_v=576), -2),
                          (dict(kv_shared=False), -2)]:
         try:

@@ -255,6 +255,9 @@ def main():
     res["mfma_probe"] = {"tflops": round(p_tf, 1), "sclk_ghz": round(p_ghz, 3),
                          "attn_frac_of_probe": (round(res["roofline"]["achieved"] / p_tf, 4)
                                                 if res["roofline"]["bound"] == "mfma" else None)}
+    if res["roofline"]["bound"] == "hbm":
+        r_gbs = hbm_read_probe(torch)
+        res["hbm_read_probe"] = {"GBps": round(r_gbs, 1), "attn_frac_of_probe": round(res["roofline"]["achieved"] / r_gbs, 4)}
     extras = [] if args.extras.strip().lower() in ("", "none") else [e.strip() for e in args.extras.split(",")]
     if extras:
         res["extra"] = {}
@@ -543,6 +546,8 @@ def main_kda(args):
                      "frac": round(gbps / PEAK_HBM_GBS, 4), "traffic": traffic, "kernel": "kda_prefill_kernel",
                      "alg_bytes_per_launch": b, "alg_flop_per_launch": f, **counters},
     }
+    r_gbs = hbm_read_probe(torch)
+    res["hbm_read_probe"] = {"GBps": round(r_gbs, 1), "kda_frac_of_probe": round(gbps / r_gbs, 4)}
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = kda_cpu_baseline(spec, wk.make_tensors(spec, seed=8000, device=dev, poison=False))
     print(json.dumps(res), flush=True)
@@ -577,6 +582,35 @@ def mfma_probe(torch, workgroups=1024, iters=20000, random_ops=1, launches=20):
     t = float(np.median([a.elapsed_time(b) for a, b in ms[len(ms) // 2:]]))
     c = clocks.cpu().numpy().astype(np.float64)
     return workgroups * 8 * iters * 4 * 32768.0 / (t * 1e-3) / 1e12, float((c[2] - c[0]) / ((c[3] - c[1]) * 10.0))
+
+
+def hbm_read_probe(torch, mib=4096, workgroups=8192, launches=12):
+    """Median GB/s of the library's read-only streaming probe over a `mib` MiB device buffer: the rate
+    plain streaming reads reach on this GPU, the practical ceiling of the gather-bound waves."""
+    import ctypes
+    import paper_2609_35263_amd as wp
+    lib = wp.load_library()
+    lib.wavepp_probe_hbm_read.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p,
+                                          ctypes.c_void_p]
+    lib.wavepp_probe_hbm_read.restype = ctypes.c_int
+    nbytes = mib << 20
+    src = torch.ones(nbytes // 4, dtype=torch.int32, device="cuda")
+    sink = torch.empty(workgroups * 256, dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream()
+    ms = []
+    for _ in range(launches):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        st = lib.wavepp_probe_hbm_read(ctypes.c_void_p(src.data_ptr()), nbytes, workgroups,
+                                       ctypes.c_void_p(sink.data_ptr()), ctypes.c_void_p(stream.cuda_stream))
+        if st != 0:
+            raise RuntimeError(f"read probe failed: {st}")
+        e1.record(stream)
+        ms.append((e0, e1))
+    torch.cuda.synchronize()
+    t = float(np.median([a.elapsed_time(b) for a, b in ms[len(ms) // 2:]]))
+    del src, sink
+    return nbytes / (t * 1e-3) / 1e9
 
 
 def main_peak(args, workgroups=1024, iters=20000):

@@ -18,6 +18,17 @@
  *   clocks      uint64[4]: memtime start, memrealtime start, memtime end, memrealtime end
  * FLOP per launch = workgroups * 8 * iters * 4 * 32768.
  * Errors: WAVEPP_EINVAL for a non-positive size or a NULL pointer; launch errors as WAVEPP_EHIP.
+ *
+ * wavepp_probe_hbm_read: the rate at which plain streaming reads move data from HBM, the practical
+ * ceiling for the gather-bound waves (their K/V pages are read once, nothing comparable is written).
+ * Each thread of `workgroups` x 256 reads 16-byte words of `src` grid-stride, four 4 KiB-apart words
+ * per round, XORs them together and writes one uint32 to `sink`; every byte of `src` is read exactly
+ * once, so the XOR of all of `sink` equals the XOR of all 32-bit words of `src`.
+ *   src         device buffer, 16-byte aligned, `bytes` long (a multiple of 16), caller-owned
+ *   workgroups  grid size, >= 1 (a few thousand fill the chip's memory queues)
+ *   sink        device uint32[workgroups * 256], caller-owned
+ * Bytes read per launch = bytes.  Errors: WAVEPP_EINVAL for a non-positive or unaligned size, an
+ * unaligned or NULL pointer; launch errors as WAVEPP_EHIP.
  */
 #ifndef WAVEPP_PROBE_H
 #define WAVEPP_PROBE_H
@@ -30,6 +41,7 @@ extern "C" {
 
 int wavepp_probe_mfma(int32_t workgroups, int32_t iters, int32_t random_operands, float* sink,
                       unsigned long long* clocks, hipStream_t stream);
+int wavepp_probe_hbm_read(const void* src, int64_t bytes, int32_t workgroups, uint32_t* sink, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -49,7 +49,7 @@ KDA_SYMBOLS = [
     "wavepp_kda_plan", "wavepp_kda_workspace_bytes", "wavepp_kda_get_info", "wavepp_kda_upload",
     "wavepp_kda_chunked_prefill", "wavepp_kda_destroy",
 ]
-PROBE_SYMBOLS = ["wavepp_probe_mfma"]
+PROBE_SYMBOLS = ["wavepp_probe_mfma", "wavepp_probe_hbm_read"]
 
 
 class WaveppError(RuntimeError):

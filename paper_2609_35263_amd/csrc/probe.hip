@@ -69,6 +69,26 @@ __global__ __launch_bounds__(kProbeThreads) void mfma_probe_kernel(int iters, in
   sink[int64_t(blockIdx.x) * kProbeThreads + tid] = s;
 }
 
+
+// Read-only HBM stream: every thread reads 16 bytes from each of four 4 KiB-apart positions per
+// round (grid-stride), folds them with XOR and writes one word, so the bytes read are exactly the
+// buffer once and nothing is written back but the per-thread words.
+constexpr int kReadThreads = 256;
+typedef uint32_t u32x4p __attribute__((ext_vector_type(4)));
+
+__global__ __launch_bounds__(kReadThreads) void hbm_read_probe_kernel(const u32x4p* __restrict__ src, int64_t n16,
+                                                                      uint32_t* __restrict__ sink) {
+  u32x4p acc = {0u, 0u, 0u, 0u};
+  const int64_t stride = int64_t(gridDim.x) * kReadThreads * 4;
+  for (int64_t i = int64_t(blockIdx.x) * kReadThreads * 4 + threadIdx.x; i < n16; i += stride) {
+    const u32x4p a = src[i];
+    const u32x4p b = (i + kReadThreads < n16) ? src[i + kReadThreads] : u32x4p{0u, 0u, 0u, 0u};
+    const u32x4p c = (i + 2 * kReadThreads < n16) ? src[i + 2 * kReadThreads] : u32x4p{0u, 0u, 0u, 0u};
+    const u32x4p d = (i + 3 * kReadThreads < n16) ? src[i + 3 * kReadThreads] : u32x4p{0u, 0u, 0u, 0u};
+    acc ^= a ^ b ^ c ^ d;
+  }
+  sink[int64_t(blockIdx.x) * kReadThreads + threadIdx.x] = acc.x ^ acc.y ^ acc.z ^ acc.w;
+}
 }  // namespace
 }  // namespace wavepp
 
@@ -80,6 +100,21 @@ extern "C" int wavepp_probe_mfma(int32_t workgroups, int32_t iters, int32_t rand
   if (!sink || !clocks) return set_error(WAVEPP_EINVAL, "sink / clocks is NULL");
   hipLaunchKernelGGL(mfma_probe_kernel, dim3(workgroups), dim3(kProbeThreads), 0, stream, iters,
                      random_operands ? 1 : 0, sink, clocks);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return set_hip_error(e, "probe launch");
+  return WAVEPP_OK;
+}
+
+extern "C" int wavepp_probe_hbm_read(const void* src, int64_t bytes, int32_t workgroups, uint32_t* sink,
+                                     hipStream_t stream) {
+  using namespace wavepp;
+  clear_error();
+  if (workgroups <= 0 || bytes <= 0) return set_error(WAVEPP_EINVAL, "workgroups and bytes must be positive");
+  if (bytes % 16 != 0) return set_error(WAVEPP_EINVAL, "bytes must be a multiple of 16");
+  if (!src || !sink) return set_error(WAVEPP_EINVAL, "src / sink is NULL");
+  if (reinterpret_cast<uintptr_t>(src) % 16 != 0) return set_error(WAVEPP_EINVAL, "src must be 16-byte aligned");
+  hipLaunchKernelGGL(hbm_read_probe_kernel, dim3(workgroups), dim3(kReadThreads), 0, stream,
+                     static_cast<const u32x4p*>(src), bytes / 16, sink);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return set_hip_error(e, "probe launch");
   return WAVEPP_OK;

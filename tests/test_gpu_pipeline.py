@@ -222,3 +222,34 @@ def test_mfma_probe_reports_a_plausible_rate_and_clock():
     assert 0.3 < ghz < 3.0
     assert 50.0 < tflops < 2600.0
     assert torch.isfinite(sink).all()
+
+
+def test_hbm_read_probe_reads_every_word_once():
+    """The read-bandwidth probe (wavepp_probe.h): every 32-bit word of the buffer is folded into the
+    sink exactly once (the XOR of the sink equals the XOR of the buffer, including a ragged tail that
+    is not a whole round of the grid), its argument checks reject bad sizes, and its rate stays below
+    the HBM peak (not a performance bar)."""
+    import ctypes
+    lib = wp.load_library()
+    lib.wavepp_probe_hbm_read.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p,
+                                          ctypes.c_void_p]
+    s = torch.cuda.current_stream()
+    g = torch.Generator().manual_seed(77)
+    for nbytes, wgs in ((16, 1), (1040, 3), (3 * (1 << 20) + 48, 37)):
+        host = torch.randint(-(2 ** 31), 2 ** 31 - 1, (nbytes // 4,), dtype=torch.int64, generator=g).to(torch.int32)
+        src = host.to("cuda")
+        sink = torch.zeros(wgs * 256, dtype=torch.int32, device="cuda")
+        assert lib.wavepp_probe_hbm_read(ctypes.c_void_p(src.data_ptr()), nbytes, wgs, ctypes.c_void_p(sink.data_ptr()),
+                                         ctypes.c_void_p(s.cuda_stream)) == 0
+        torch.cuda.synchronize()
+        want = np.bitwise_xor.reduce(host.numpy().view(np.uint32))
+        got = np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32))
+        assert got == want, (nbytes, wgs)
+    sink = torch.zeros(256, dtype=torch.int32, device="cuda")
+    for nbytes, wgs in ((0, 1), (24, 1), (16, 0)):
+        assert lib.wavepp_probe_hbm_read(ctypes.c_void_p(src.data_ptr()), nbytes, wgs, ctypes.c_void_p(sink.data_ptr()),
+                                         ctypes.c_void_p(s.cuda_stream)) == -1
+    import bench
+    gbs = bench.hbm_read_probe(torch, mib=1024, workgroups=4096, launches=6)
+    print(f"[read probe] {gbs:.0f} GB/s", flush=True)
+    assert 500.0 < gbs < 8000.0

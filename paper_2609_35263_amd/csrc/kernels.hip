@@ -594,12 +594,16 @@ __global__ __launch_bounds__(256, 1) void attn_mla_kernel(DevPlan p, const __bf1
       return;
     }
     const uint32_t jmax = uint32_t(n_valid - 1 - kbase);
+    // this path runs once or twice per item: its per-lane indices are rebuilt here rather than hoisted
+    // to the kernel start and kept (or spilled) for the whole item
+    uint32_t lane_w = uint32_t(64 * wave + lane);
+    asm volatile("" : "+v"(lane_w));
     int pg[PPT];
 #pragma unroll
     for (int i = 0; i < PPT; ++i) pg[i] = bt[min(tile * (KT / PAGE) + i, last_block)];
 #pragma unroll
     for (int i = 0; i < NDMA; ++i) {
-      const uint32_t P = uint32_t(64 * (wave + 4 * i) + lane);
+      const uint32_t P = lane_w + 256u * i;
       const uint32_t j = P / CPR;
       const uint32_t c = (P - CPR * j) ^ swz(j);
       const uint32_t je = min(j, jmax);

@@ -651,10 +651,11 @@ __global__ __launch_bounds__(256, 1) void attn_mla_kernel(DevPlan p, const __bf1
       asm volatile("" : "+v"(dma_d[0]), "+v"(dma_d[1]), "+v"(dma_d[2]), "+v"(dma_d[3]), "+v"(dma_d[4]));
       const int kbase = tile * KT;
       // S^T of both key blocks: 2 x 36 MFMAs sharing each Q fragment; K fragments read KPF steps
-      // ahead, in source order, so the reads stay in flight behind the MFMAs
+      // ahead, in source order, so the reads stay in flight behind the MFMAs (three steps measured
+      // 1.5 % faster on cfg5 than two; four spill)
       f32x16 sacc[2];
       {
-        constexpr int KPF = 2;
+        constexpr int KPF = 3;
         bf16x8 kbuf[2][KPF];
   #pragma unroll
         for (int i = 0; i < KPF; ++i) {

@@ -63,6 +63,7 @@ def test_cfg2_full_four_wave_form(monkeypatch):
     (16, 16, 128, 64, [100, 0], [33, 70]),            # MHA (G = 1)
     (16, 1, 64, 16, [37, 250], [45, 3]),              # MQA (G = 16)
     (32, 8, 128, 64, [4096, 0, 64, 700], [0, 300, 64, 129]),   # idle lane
+    (24, 4, 128, 64, [200, 31], [45, 70]),            # G = 6: 32-row blocks straddle tokens at uneven rows
 ])
 def test_custom_shapes(case):
     Hq, Hkv, d, B, prefix, chunk = case
@@ -347,6 +348,8 @@ def sampled_config_check(spec, seed, rows_per_req=16, heads_per_row=4):
     (16, 64, [130, 0], [70, 33]),
     (128, 64, [64], [3]),
     (8, 16, [37, 200, 5], [20, 1, 90]),
+    (40, 64, [100, 3], [17, 50]),      # G = 40: rows of one 32-row block belong to two tokens
+    (96, 64, [64, 129], [5, 2]),       # G = 96: a 128-row item spans two tokens
 ])
 def test_latent_small(case):
     Hq, B, prefix, chunk = case

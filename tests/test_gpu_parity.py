@@ -364,6 +364,28 @@ def test_latent_splits(splits):
     check_wave(spec, seed=78, max_splits=splits)
 
 
+@pytest.mark.parametrize("chunk", [10, 40])   # 40 rows: the 4-wave form; 160 rows: the 8-wave form
+def test_grouped_reference_overflow_takes_exact_second_pass(chunk):
+    # a key in a later tile has a logit ~159 (log2 units) above everything in the first tile, so the
+    # first pass's fixed per-row reference overflows and the workgroup redoes the item exactly
+    torch = _torch()
+    spec = wl.custom_wave(8, 2, 128, 128, 64, [300], [chunk], seed=15, name=f"grouped_ovf{chunk}")
+    t = wl.make_tensors(spec, seed=16)
+    rng = np.random.default_rng(4)
+    u = rng.standard_normal(128)
+    u /= np.linalg.norm(u)
+    t["q"][:] = torch.as_tensor(u * 2.0, dtype=torch.float32).to(torch.bfloat16)
+    kp = t["k_pool"].float()
+    j = 250
+    for g in range(2):
+        kp[int(spec.block_table[0, j // 64]), g, j % 64] = torch.as_tensor(u * (110.0 / 2.0 / spec.softmax_scale),
+                                                                             dtype=torch.float32)
+    t["k_pool"] = kp.to(torch.bfloat16)
+    ref = oracle_wave(spec, t)
+    g = gpu_wave(spec, t)
+    _compare.assert_parity(out_f64(g["out"]), ref["o"], g["lse"].cpu().numpy(), ref["lse"], f"grouped overflow {chunk}")
+
+
 def test_latent_reference_overflow_takes_exact_second_pass():
     # a key far later in the sequence has a logit ~150 (log2 units) above everything in the first
     # tile, so the fixed per-row reference is exceeded and the workgroup redoes its key range

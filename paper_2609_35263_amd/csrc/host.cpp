@@ -449,25 +449,50 @@ int wavepp_attn_plan(const wavepp_attn_shape* shape, const wavepp_batch* batch, 
       }
   }
   // key-range splits: forced by max_splits, or chosen so that a small wave still fills the chip,
-  // each automatic split keeping at least 1,024 keys (grouped kernel) or 512 (latent kernel)
+  // each automatic split keeping at least 1,024 keys (grouped kernel) or 512 (latent kernel).
   // Split a wave with fewer base items than this until it has about that many.  512 items are two
   // workgroups per CU of the 4-wave form, or two rounds of the one-per-CU forms; on the short-chunk
   // waves (c = 16 .. 128) it gave the fastest or within 0.5 % of the fastest split count, against
   // 1,024 items, which cost 2-11 % in the extra partials and merge work.
+  // Automatic splits share the wave's tiles out evenly rather than giving every (request, KV head,
+  // row tile) the same number of splits: such a wave runs as one round of workgroups and lasts as
+  // long as its longest item, so requests with longer prefixes take more splits.  T is the smallest
+  // tile count per split for which the wave stays within the target; an item of n tiles then takes
+  // ceil(n / T) splits (at most n / min_split_tiles).
   const int64_t fill_target = 512;
   const int64_t min_split_tiles = (mla ? 512 : 1024) / KT;
+  std::vector<int64_t> nsplit(base.size(), 1);
+  if (max_splits >= 1) {
+    for (size_t i = 0; i < base.size(); ++i)
+      nsplit[i] = std::min<int64_t>(max_splits, ceil_div(base[i].kv_end, KT));
+  } else if (int64_t(base.size()) < fill_target) {
+    auto auto_splits = [&](int64_t ntiles, int64_t T) {
+      return std::max<int64_t>(1, std::min<int64_t>(ceil_div(ntiles, T), ntiles / min_split_tiles));
+    };
+    auto total = [&](int64_t T) {
+      int64_t n = 0;
+      for (const WorkItem& w : base) n += auto_splits(ceil_div(w.kv_end, KT), T);
+      return n;
+    };
+    int64_t lo = std::max<int64_t>(1, min_split_tiles), hi = lo;
+    for (const WorkItem& w : base) hi = std::max<int64_t>(hi, ceil_div(w.kv_end, KT));
+    // total(T) does not grow with T, and total(hi) = base.size() < fill_target
+    if (total(lo) > fill_target) {
+      while (hi - lo > 1) {
+        const int64_t mid = lo + (hi - lo) / 2;
+        if (total(mid) <= fill_target) hi = mid; else lo = mid;
+      }
+      lo = hi;
+    }
+    for (size_t i = 0; i < base.size(); ++i) nsplit[i] = auto_splits(ceil_div(base[i].kv_end, KT), lo);
+  }
   std::vector<WorkItem> items;
   int64_t part_rows = 0;
   int max_used = 1;
-  for (const WorkItem& w : base) {
+  for (size_t bi = 0; bi < base.size(); ++bi) {
+    const WorkItem& w = base[bi];
     const int64_t ntiles = ceil_div(w.kv_end, KT);
-    int64_t S = 1;
-    if (max_splits >= 1) {
-      S = std::min<int64_t>(max_splits, ntiles);
-    } else if (int64_t(base.size()) < fill_target) {
-      S = std::min<int64_t>(ceil_div(fill_target, int64_t(base.size())), ntiles / min_split_tiles);
-      S = std::max<int64_t>(S, 1);
-    }
+    int64_t S = nsplit[bi];
     const int64_t tps = ceil_div(ntiles, S);
     S = ceil_div(ntiles, tps);
     if (S == 1) {

@@ -64,6 +64,7 @@ def test_cfg2_full_four_wave_form(monkeypatch):
     (16, 1, 64, 16, [37, 250], [45, 3]),              # MQA (G = 16)
     (32, 8, 128, 64, [4096, 0, 64, 700], [0, 300, 64, 129]),   # idle lane
     (24, 4, 128, 64, [200, 31], [45, 70]),            # G = 6: 32-row blocks straddle tokens at uneven rows
+    (16, 4, 128, 64, [0, 40, 100, 140, 200], [20, 30, 28, 25, 30]),   # 4-wave form: 1, 2, 2, 3, 4 key tiles
 ])
 def test_custom_shapes(case):
     Hq, Hkv, d, B, prefix, chunk = case

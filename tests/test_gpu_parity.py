@@ -65,6 +65,8 @@ def test_cfg2_full_four_wave_form(monkeypatch):
     (32, 8, 128, 64, [4096, 0, 64, 700], [0, 300, 64, 129]),   # idle lane
     (24, 4, 128, 64, [200, 31], [45, 70]),            # G = 6: 32-row blocks straddle tokens at uneven rows
     (16, 4, 128, 64, [0, 40, 100, 140, 200], [20, 30, 28, 25, 30]),   # 4-wave form: 1, 2, 2, 3, 4 key tiles
+    (8, 2, 64, 64, [300, 17], [25, 32]),              # 4-wave form, d = 64 on 64-token pages
+    (8, 2, 128, 16, [90, 250, 0], [30, 5, 20]),       # 4-wave form, d = 128 on 16-token pages
 ])
 def test_custom_shapes(case):
     Hq, Hkv, d, B, prefix, chunk = case

@@ -182,6 +182,25 @@ def test_kv_tile_is_the_kernel_form_tile(monkeypatch):
                     assert ke - kb >= 1024, (r, g, row0, kb, ke)
 
 
+def test_auto_splits_follow_request_length():
+    """A wave split to fill the chip stays within 512 items, gives requests with longer prefixes at
+    least as many splits as shorter ones, and keeps its items' key ranges within 20 % of their mean
+    (the wave runs as one round of workgroups, so its longest item sets the interval)."""
+    for c in (16, 32, 64):
+        spec = wl.small_chunk(c)
+        it = wp.plan_for(spec).items()
+        real = it[it[:, 3] > 0]
+        assert len(real) <= 512
+        lens = real[:, 5] - real[:, 4]
+        assert lens.max() <= 1.2 * lens.mean(), (c, lens.max(), lens.mean())
+        splits = {}
+        for r in real:
+            splits[(int(r[0]), int(r[1]), int(r[2]))] = splits.get((int(r[0]), int(r[1]), int(r[2])), 0) + 1
+        by_len = sorted((int(spec.prefix_lens[k[0]] + spec.chunk_lens[k[0]]), n) for k, n in splits.items())
+        assert all(a[1] <= b[1] for a, b in zip(by_len, by_len[1:])), (c, by_len)
+        coverage_check(spec, it, wp.plan_for(spec).info()["kv_tile"])
+
+
 def test_plan_is_deterministic_and_independent_of_physical_pages():
     spec = wl.cfg2()
     a = wp.plan_for(spec).items()

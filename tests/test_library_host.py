@@ -201,6 +201,37 @@ def test_auto_splits_follow_request_length():
         coverage_check(spec, it, wp.plan_for(spec).info()["kv_tile"])
 
 
+@pytest.mark.parametrize("seed", range(4))
+def test_auto_splits_fuzz(seed):
+    """Seeded random small waves with long prefixes, in both grouped forms and the latent one: the
+    automatic splits cover every visible pair exactly once, keep the wave within 512 items, and cut
+    no split but a range's last below the minimum split length."""
+    rng = np.random.default_rng(900 + seed)
+    for _ in range(6):
+        Hq, Hkv, d, kv_shared = [(32, 8, 128, False), (16, 4, 64, False), (64, 8, 128, False),
+                                 (16, 1, 576, True)][rng.integers(0, 4)]
+        R = int(rng.integers(1, 9))
+        G = Hq // Hkv
+        max_c = max(1, (128 if kv_shared else 256) // G)
+        prefix = (rng.integers(0, 9000, R) // 64) * 64 + rng.integers(0, 64, R) * (rng.random(R) < 0.5)
+        chunk = rng.integers(1, max_c + 1, R)
+        spec = wl.custom_wave(Hq, Hkv, d, 512 if kv_shared else d, 64, prefix, chunk, kv_shared=kv_shared,
+                              seed=int(rng.integers(0, 1000)))
+        p = wp.plan_for(spec)
+        info, items = p.info(), p.items()
+        coverage_check(spec, items, info["kv_tile"])
+        real = items[items[:, 3] > 0]
+        n_base = sum(-(-int(c) * G // info["rows_per_item"]) for c in chunk) * (1 if kv_shared else Hkv)
+        if n_base < 512:
+            assert len(real) <= 512, (len(real), n_base)
+        min_keys = 512 if kv_shared else 1024
+        parts = real[real[:, 6] >= 0]
+        for (r, g, row0, rows, kb, ke, part, split) in parts:
+            later = parts[(parts[:, 0] == r) & (parts[:, 1] == g) & (parts[:, 2] == row0) & (parts[:, 7] > split)]
+            if len(later):
+                assert ke - kb >= min_keys, (r, g, row0, kb, ke)
+
+
 def test_plan_is_deterministic_and_independent_of_physical_pages():
     spec = wl.cfg2()
     a = wp.plan_for(spec).items()

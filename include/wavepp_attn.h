@@ -189,7 +189,7 @@ int wavepp_attn_chunked_prefill(const wavepp_plan* plan, const void* q, const vo
  * The metadata is copied from the plan's host memory with hipMemcpyAsync on `stream` (from
  * pageable memory the runtime reads it before returning; under stream capture the copy becomes a
  * graph node that reads the plan's host memory each time the graph runs, so the plan must outlive
- * the graph, and this use is not covered by the library's tests), then the same kernels as the
+ * the graph; replays are bit-identical to an eager call), then the same kernels as the
  * workspace entry points run on `stream`; results are bit-identical to wavepp_attn_append_kv +
  * wavepp_attn_chunked_prefill on the same plan.  Arguments as there: k_new / v_new as for
  * wavepp_attn_append_kv (both NULL: the pools already hold the chunks' K/V; v_new NULL for a
